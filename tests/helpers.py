@@ -48,3 +48,65 @@ def allclose_report(got, ref, atol, rtol):
     return dict(ok=not bad.any(), n_bad=int(bad.sum()), max_abs=float(err.max(initial=0.0)),
                 max_rel=float((err / np.maximum(np.abs(ref), 1e-30)).max(initial=0.0)),
                 rms=float(np.sqrt(np.mean(err ** 2))) if err.size else 0.0)
+
+
+# ----------------------------------------------------------------------------- GPU-side glue
+def advance_head(ring, n, base_id=10 ** 9):
+    """Move the ring's rotation head by n slots (acquire and release placeholder requests)."""
+    for i in range(n):
+        ring.append(base_id + i, 1)
+        ring.release(base_id + i)
+
+
+def reserve_step(ring, specs):
+    """Reserve one packed step.  specs: list of (request_id, pos0, q_len) in packing order;
+    a request not yet resident first gets pos0 positions of history.  Returns segment tuples
+    (q_start, q_len, slot, pos0, request_id, flags)."""
+    import paper_2512_20276_amd as af
+    segs, row = [], 0
+    for rid, pos0, q_len in specs:
+        owners, lens, _ = ring.state()
+        if rid not in owners and pos0 > 0:
+            ring.append(rid, pos0)
+        s = ring.append(rid, q_len)
+        assert s.pos0 == pos0, (rid, s.pos0, pos0)
+        segs.append((row, q_len, s.slot, s.pos0, rid, af.AF_SEG_EMIT))
+        row += q_len
+    return segs
+
+
+def oracle_segments(segs):
+    import oracle
+    return [oracle.Segment(q_start=s[0], q_len=s[1], slot=s[2], pos0=s[3], request_id=s[4],
+                           emit=bool(s[5] & 1)) for s in segs]
+
+
+def gpu_shape_weights(shape, seed=0, random_gains=False):
+    """Seeded weights drawn on the GPU (fast for the 7B shape)."""
+    return wl.model_weights(shape, seed=seed, device="cuda", random_gains=random_gains)
+
+
+def bf16_layer_parity(got, ref, atol=2e-2, rtol=1e-2, outlier_frac=1e-4, norm_rel=1e-2):
+    """Parity of bf16 hidden states that went through a whole layer (or more).
+
+    Every stored intermediate is rounded to bf16 on both sides, so an fp32-vs-float64
+    accumulation difference that moves one value across a rounding boundary changes it by an
+    ulp, and later layers mix such flips into many elements.  Measured on one 7B layer: the
+    attention output is 98.9% bit-identical, the residual after the MLP 57%.  Where the
+    residual update cancels a large input, a one-ulp flip of the large term remains as an
+    absolute error on a small result.  The bound therefore has two parts:
+      normwise   ||got - ref||_2 <= norm_rel * ||ref||_2                 (rel 1e-2)
+      elementwise |got - ref| <= atol + rtol |ref| for all but outlier_frac of the elements
+                                                                       (max-abs 2e-2 / rel 1e-2)
+    Single steps on identical inputs are held to the elementwise bound with no outliers."""
+    rep = allclose_report(got, ref, atol, rtol)
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    rep["norm_rel"] = float(np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30))
+    rep["outlier_frac"] = rep["n_bad"] / max(ref.size, 1)
+    rep["ok"] = rep["norm_rel"] <= norm_rel and rep["outlier_frac"] <= outlier_frac
+    return rep
+
+
+def exact_fraction(got, ref):
+    return float(np.mean(np.asarray(got, dtype=np.float64) == np.asarray(ref, dtype=np.float64)))

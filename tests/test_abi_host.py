@@ -1,0 +1,135 @@
+"""CPU tests of the C ABI: the library loads, exports every declared entry point, and its
+slot bookkeeping (a bookkeeping-only ring, no device call) matches the oracle's RingModel
+bit for bit, errors included."""
+import os
+import random
+import re
+
+import pytest
+
+import paper_2512_20276_amd as af
+from oracle.ring import RingError, RingModel
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "actionflow.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[A-Za-z_][\w\s\*]*?\b(af_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_contract():
+    names = declared_functions()
+    for must in ("af_ring_create", "af_ring_append", "af_ring_release", "af_packed_forward",
+                 "af_packed_layer_forward", "af_weights_create", "af_last_error"):
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol():
+    missing = [n for n in declared_functions() if not hasattr(af.lib, n)]
+    assert not missing, missing
+
+
+def test_tensor_count():
+    assert af.lib.af_weights_tensor_count(32) == 3 + 9 * 32
+
+
+def _pipeline_ops(K, L_P, steps):
+    ops = []
+    ntok = {}
+    for t in range(steps):
+        for s in range(K):
+            r = t - s
+            if r < 0:
+                break
+            ops.append(("append", r, L_P if s == 0 else 1))
+            ntok[r] = ntok.get(r, 0) + 1
+        for r in [r for r, c in ntok.items() if c == K]:
+            ops.append(("release", r, 0))
+            del ntok[r]
+    return ops
+
+
+def _apply(ring, model, op):
+    kind, rid, n = op
+    got = want = None
+    try:
+        if kind == "append":
+            s = ring.append(rid, n)
+            got = (s.slot, s.pos0, s.q_len, s.request_id)
+        else:
+            ring.release(rid)
+            got = "ok"
+    except af.AFError as e:
+        got = ("err", e.code)
+    try:
+        if kind == "append":
+            slot, pos0 = model.append(rid, n)
+            want = (slot, pos0, n, rid)
+        else:
+            model.release(rid)
+            want = "ok"
+    except RingError as e:
+        want = ("err", e.code)
+    return got, want
+
+
+@pytest.mark.parametrize("K,n_slots", [(7, 8), (3, 4), (8, 64), (7, 7)])
+def test_pipeline_schedule_bit_exact_vs_oracle(K, n_slots):
+    ring = af.Ring(0, n_slots, 288)
+    model = RingModel(n_slots, 288)
+    for op in _pipeline_ops(K, 276, 64):
+        got, want = _apply(ring, model, op)
+        assert got == want, op
+        owners, lens, head = ring.state()
+        assert (owners, lens, head) == model.state()
+    ring.close()
+
+
+def test_random_schedules_bit_exact_vs_oracle():
+    rnd = random.Random(7)
+    for n_slots, max_pos in ((1, 3), (2, 5), (3, 8), (5, 2)):
+        ring, model = af.Ring(0, n_slots, max_pos), RingModel(n_slots, max_pos)
+        ids = []
+        for i in range(400):
+            r = rnd.random()
+            if r < 0.4:
+                op = ("append", len(ids) + 100, rnd.randint(-1, max_pos + 1))
+                ids.append(op[1])
+            elif r < 0.8 and ids:
+                op = ("append", rnd.choice(ids), rnd.randint(-1, 3))
+            elif ids:
+                op = ("release", rnd.choice(ids + [10 ** 9]), 0)
+            else:
+                continue
+            got, want = _apply(ring, model, op)
+            assert got == want, (i, op)
+            assert ring.state() == model.state()
+
+
+def test_error_codes_and_messages():
+    ring = af.Ring(0, 2, 8)
+    ring.append(5, 8)
+    with pytest.raises(af.AFError) as e:
+        ring.append(5, 1)
+    assert e.value.code == af.AF_ERR_OUT_OF_RANGE and "max_pos" in str(e.value)
+    ring.append(6, 1)
+    with pytest.raises(af.AFError) as e:
+        ring.append(7, 1)
+    assert e.value.code == af.AF_ERR_SLOT_BUSY
+    with pytest.raises(af.AFError) as e:
+        ring.release(99)
+    assert e.value.code == af.AF_ERR_UNKNOWN_REQUEST
+    with pytest.raises(af.AFError) as e:
+        ring.append(8, 0)
+    assert e.value.code == af.AF_ERR_INVALID_ARG
+    ring.reset()
+    assert ring.state() == ([-1, -1], [0, 0], 0)
+
+
+def test_ring_create_rejects_bad_descriptors():
+    for args in ((0, 0, 8), (0, 4, 0), (-1, 4, 8)):
+        with pytest.raises(af.AFError) as e:
+            af.Ring(*args)
+        assert e.value.code == af.AF_ERR_INVALID_ARG
