@@ -1,0 +1,236 @@
+#!/usr/bin/env python3
+"""Throughput of the Cross-Request State Packed Forward on one MI355X.
+
+Workload (default): the steady-state cross-request pipeline of a 32-layer Llama-2-7B-shape
+decoder in bf16 (d 4096, 32 heads x 128, SwiGLU 11008, vocab 32000), action length K = 7:
+every step packs one new 276-row prefill (256 N(0,1) "vision" rows + 20 instruction token
+ids) with the 6 single decode rows of the requests in flight (M = 282 rows), runs all 32
+layers over a ring of 8 slots x 288 positions (slots wrap every 8 steps), and emits 7 greedy
+tokens through the LM head.  Weights are random N(0, 0.02) (seeded draws on the GPU).
+
+One "step" is one packed forward (af_packed_forward) plus its host bookkeeping; W warm-up
+steps (>= K - 1 so every timed step is a full M = 282 step), then K timed steps bracketed by
+device synchronizations.  A second pass over the same number of steps records HIP events
+around every kernel launch (on the launch stream) for the per-kernel roofline figures.
+
+Prints one JSON line (stdout); progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "packed tokens/s + packed steps/s at 7B shape; % MFMA bf16 peak, % HBM BW"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=30)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
+    p.add_argument("--no-timing-pass", action="store_true")
+    return p.parse_args()
+
+
+# ----------------------------------------------------------------------------- algorithmic work
+def gemm_work(M, D, F, V, n_emit):
+    """Per-launch algorithmic flops and bytes (weights once, activations in and out, bf16)."""
+    b = 2
+    w = {
+        "gemm_qkv": (2 * M * D * 3 * D, b * (3 * D * D + M * D + 3 * M * D)),
+        "gemm_o": (2 * M * D * D, b * (D * D + M * D + 2 * M * D)),
+        "gemm_gateup": (2 * M * D * 2 * F, b * (2 * F * D + M * D + M * F)),
+        "gemm_down": (2 * M * F * D, b * (D * F + M * F + 2 * M * D)),
+        "lm_head": (2 * n_emit * D * V, b * (V * D + n_emit * D) + 4 * n_emit * V),
+    }
+    return w
+
+
+def attention_bytes(segs, H, hd):
+    """Keys and values each row's segment reads (its slot, positions 0..kv_len-1), plus Q in and O out."""
+    b = 2
+    kv = sum((s[3] + s[1]) * H * hd * 2 * b for s in segs)
+    M = sum(s[1] for s in segs)
+    return kv + 2 * M * H * hd * b
+
+
+# ----------------------------------------------------------------------------- cpu baseline
+def cpu_baseline(seconds_budget: float):
+    """The oracle (float64 NumPy, as it stands) on a bounded sample of the same workload: one
+    steady-state packed step (276 prefill rows + 6 decode rows, contexts 277..282) through as
+    many 7B-shape layers as fit the time budget (at least one), extrapolated to 32 layers plus
+    the final norm / LM head of the 7 emitting rows."""
+    import numpy as np
+    import torch
+    import threadpoolctl
+
+    import oracle
+    import workload as wl
+
+    shape = wl.LLAMA7B
+    H, hd, D = shape.n_heads, shape.head_dim, shape.d_model
+    to64 = lambda t: t.detach().to("cpu", torch.float64).numpy()
+    layers = [{k: to64(v) for k, v in wl.layer_weights(shape, l, seed=0, device="cuda").items()} for l in range(2)]
+    glob = {k: to64(v) for k, v in wl.global_weights(shape, seed=0, device="cuda").items()}
+    torch.cuda.empty_cache()
+    model = oracle.OracleModel(shape.with_layers(2), glob, layers, storage="bf16")
+    rng = np.random.default_rng(0)
+    kv = oracle.OracleRingKV(2, 8, 288, H, hd)
+    segs = [oracle.Segment(0, 276, 2, 0, 10)] + [oracle.Segment(276 + s - 1, 1, (2 - s) % 8, 276 + s - 1, 10 - s)
+                                                 for s in range(1, 7)]
+    for i, sg in enumerate(segs):
+        sg.q_start = 0 if i == 0 else 276 + i - 1
+        if sg.pos0:
+            kv.k[:, sg.slot, :sg.pos0] = rng.standard_normal((2, sg.pos0, H, hd))
+            kv.v[:, sg.slot, :sg.pos0] = rng.standard_normal((2, sg.pos0, H, hd))
+    x = oracle.round_storage(rng.standard_normal((282, D)), "bf16")
+    info = threadpoolctl.threadpool_info()
+    threads = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
+    t_layers, n = 0.0, 0
+    h = x
+    while n < 32 and (n == 0 or t_layers < seconds_budget):
+        t0 = time.perf_counter()
+        h = model.layer_packed(n % 2, h, segs, kv)
+        t_layers += time.perf_counter() - t0
+        n += 1
+        log(f"cpu oracle: layer {n} done ({t_layers:.1f} s)")
+    t0 = time.perf_counter()
+    model.logits(h[[s.q_start + s.q_len - 1 for s in segs]])
+    t_head = time.perf_counter() - t0
+    step_s = t_layers / n * 32 + t_head
+    return {"value": 282.0 / step_s, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"one 282-row packed step through {n} of 32 layers ({t_layers:.1f} s) + LM head "
+                      f"({t_head:.2f} s), extrapolated to 32 layers: {step_s:.1f} s/step",
+            "seconds_per_step": step_s}
+
+
+# ----------------------------------------------------------------------------- main
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (each MI355X would run its "
+              "own independent pipelines); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2512_20276_amd as af
+    import workload as wl
+    from paper_2512_20276_amd.pipeline import Pipeline
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = "cuda"
+    shape = wl.LLAMA7B
+    K, L_V, L_T, n_slots, max_pos = 7, 256, 20, 8, 288
+    L_P = L_V + L_T
+    M = L_P + K - 1
+    D, F, V, H, hd = shape.d_model, shape.d_ff, shape.vocab, shape.n_heads, shape.head_dim
+    if args.warmup < K - 1:
+        log(f"warm-up raised to {K - 1} so that every timed step is a full packed step")
+        args.warmup = K - 1
+
+    t0 = time.time()
+    g, layers = wl.model_weights(shape, seed=0, device=dev)
+    w = af.Weights(shape, g, layers)
+    del g, layers
+    torch.cuda.empty_cache()
+    ring = af.Ring(shape.n_layers, n_slots, max_pos, H, hd, dtype=torch.bfloat16)
+    text = wl.draw_ids(("instruction", 0), L_T, V, device=dev)
+    pids = torch.cat([torch.full((L_V,), -1, dtype=torch.int32, device=dev), text])
+    pool = []
+    for i in range(8):   # eight distinct camera frames, reused cyclically
+        e = torch.zeros((M, D), dtype=torch.bfloat16, device=dev)
+        e[:L_V] = wl.draw(("vision", 0, i), (L_V, D), device=dev)
+        pool.append(e)
+    pipe = Pipeline(w, ring, K, pids, lambda t: pool[t % len(pool)], keep_history=False)
+    torch.cuda.synchronize()
+    log(f"setup {time.time() - t0:.1f} s; warm-up {args.warmup} steps")
+
+    for _ in range(args.warmup):
+        pipe.step()
+    torch.cuda.synchronize()
+    log(f"timed: {args.steps} steps")
+    t0 = time.perf_counter()
+    Ms = []
+    for _ in range(args.steps):
+        Ms.append(pipe.step().M)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    assert all(m == M for m in Ms), Ms
+    ms_step = elapsed / args.steps * 1e3
+    steps_s = args.steps / elapsed
+    tokens_s = M * steps_s
+    log(f"{ms_step:.3f} ms/step, {tokens_s:.0f} packed tokens/s")
+
+    out = {"metric": METRIC, "value": round(tokens_s, 1), "unit": "tokens/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic (seeded N(0,1) vision rows, fixed instruction ids, random-init N(0,0.02) weights)",
+           "config": {"workload": "7B-shape 32-layer packed step, K=7 pipeline steady state: 276 prefill + 6 decode "
+                                  "rows (M=282), ring 8 slots x 288, LM head + argmax on 7 rows",
+                      "M": M, "layers": shape.n_layers, "K": K, "prefill_rows": L_P, "decode_rows": K - 1},
+           "packed_steps_per_s": round(steps_s, 3),
+           "action_tokens_per_s": round(K * steps_s, 2)}
+
+    if not args.no_timing_pass:
+        w.timing_enable((1 << af.AF_K_COUNT) - 1)
+        segs_seen = None
+        t1 = time.perf_counter()
+        for _ in range(args.steps):
+            r = pipe.step()
+            segs_seen = r.segments
+        torch.cuda.synchronize()
+        t_inst = time.perf_counter() - t1
+        tm = w.timing_read()
+        w.timing_enable(0)
+        work = gemm_work(M, D, F, V, K)
+        per_step = {k: round(ms / args.steps, 4) for k, (ms, n) in tm.items()}
+        gemm_ms = sum(tm[k][0] for k in ("gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down")) / args.steps
+        gemm_flops = sum(work[k][0] for k in ("gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down")) * shape.n_layers
+        mfma_frac = gemm_flops / (gemm_ms * 1e-3) / (PEAK_BF16_TFLOPS * 1e12)
+        ga_ms, ga_n = tm["gemm_gateup"]
+        ga_avg = ga_ms / ga_n
+        ga_flops, ga_bytes = work["gemm_gateup"]
+        ga_gbs = ga_bytes / (ga_avg * 1e-3) / 1e9
+        at_ms, at_n = tm["attention"]
+        at_bytes = attention_bytes(segs_seen, H, hd)
+        at_gbs = at_bytes / (at_ms / at_n * 1e-3) / 1e9
+        out["roofline"] = {"kernel": "gemm_kernel, SwiGLU epilogue (gate/up projection)",
+                           "bound": "hbm", "achieved": round(ga_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                           "frac": round(ga_gbs / PEAK_HBM_GBS, 4), "traffic": None,
+                           "bytes_per_launch": ga_bytes, "avg_launch_us": round(ga_avg * 1e3, 2),
+                           "tflops": round(ga_flops / (ga_avg * 1e-3) / 1e12, 1)}
+        out["mfma_frac_projection_gemms"] = round(mfma_frac, 4)
+        out["projection_gemm_tflops"] = round(gemm_flops / (gemm_ms * 1e-3) / 1e12, 1)
+        out["attention_hbm"] = {"GB/s": round(at_gbs, 1), "frac": round(at_gbs / PEAK_HBM_GBS, 4),
+                                "bytes_per_launch": at_bytes, "avg_launch_us": round(at_ms / at_n * 1e3, 2)}
+        out["kernel_ms_per_step"] = per_step
+        out["kernel_sum_ms_per_step"] = round(sum(ms for ms, _ in tm.values()) / args.steps, 4)
+        out["timing_pass_ms_per_step"] = round(t_inst / args.steps * 1e3, 4)
+        log(f"timing pass: {json.dumps(per_step)}")
+
+    ring.close()
+    w.close()
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle sample)")
+        out["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -161,6 +161,15 @@ af_status af_packed_forward(af_weights* w, const int32_t* token_ids, const void*
 af_status af_packed_layer_forward(af_weights* w, int32_t layer, void* hidden_inout, int32_t M,
                                   const af_segment* segs, int32_t n_seg, af_ring* ring, void* hip_stream);
 
+/* Options of the forward (bit flags; default 0):
+ *  AF_OPT_NO_SPLIT_K  never split a projection's K range over workgroups.  Every kernel then
+ *                     computes a row exactly as it would with no other rows packed beside it
+ *                     (bit-identical), at some cost in parallelism for small packed steps.  By
+ *                     default, projections with too few output tiles to fill the GPU sum fp32
+ *                     partials over K splits (deterministic, but in another order). */
+#define AF_OPT_NO_SPLIT_K 1u
+af_status af_weights_set_options(af_weights* w, uint32_t flags);
+
 /* Copies and clears the device error counter (ids out of range) after synchronizing hip_stream. */
 af_status af_weights_device_errors(af_weights* w, void* hip_stream, int32_t* count);
 

@@ -15,12 +15,13 @@ from typing import Dict, List, Optional, Sequence
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libactionflow.so")
+LIB_PATH = os.environ.get("AF_LIBRARY_PATH") or os.path.join(_HERE, "libactionflow.so")
 
 AF_OK, AF_ERR_INVALID_ARG, AF_ERR_OUT_OF_RANGE, AF_ERR_SLOT_BUSY = 0, -1, -2, -3
 AF_ERR_UNKNOWN_REQUEST, AF_ERR_DEVICE, AF_ERR_OOM, AF_ERR_UNSUPPORTED = -4, -5, -6, -7
 AF_F32, AF_BF16 = 0, 1
 AF_SEG_EMIT = 1
+AF_OPT_NO_SPLIT_K = 1
 KERNEL_CLASSES = ["embed", "rmsnorm", "gemm_qkv", "attention", "gemm_o", "gemm_gateup", "gemm_down",
                   "lm_head", "argmax"]
 AF_K_COUNT = len(KERNEL_CLASSES)
@@ -88,6 +89,7 @@ def _load():
         "af_op_gate_up_swiglu": (I32, [P, I32, P, P, I32, P]),
         "af_op_down_residual": (I32, [P, I32, P, P, I32, P]),
         "af_op_lm_head_argmax": (I32, [P, P, I32, SEG, I32, P, P, P]),
+        "af_weights_set_options": (I32, [P, U32]),
         "af_timing_enable": (I32, [P, U32]),
         "af_timing_read": (I32, [P, C.POINTER(C.c_double), C.POINTER(I64)]),
     }
@@ -239,6 +241,9 @@ class Weights:
         c = C.c_int32()
         _check(lib.af_weights_device_errors(self.h, _stream(stream), C.byref(c)))
         return c.value
+
+    def set_options(self, flags: int):
+        _check(lib.af_weights_set_options(self.h, flags))
 
     def timing_enable(self, mask: int):
         _check(lib.af_timing_enable(self.h, mask))

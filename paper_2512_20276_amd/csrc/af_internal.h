@@ -43,9 +43,12 @@ enum Epi { EPI_STORE = 0, EPI_STORE_F32 = 1, EPI_RESID = 2, EPI_SWIGLU = 3, EPI_
 
 struct GemmArgs {
   const void* A;  // [M, K] activations, row stride lda elements
-  const void* B;  // [N, K] weights, row stride ldb elements
-  int M, N, K, lda, ldb;
-  void* out;      // EPI_STORE/_F32/_RESID: [M, N]; EPI_SWIGLU: [M, N/2]; EPI_QKV: queries [M, d_model]
+  const void* B;  // weights, fragment-tiled: n-block nb at B + nb * bstride, [Kp/32][64][8] each
+  int M, N, K, Kp, lda;
+  long bstride;    // elements between consecutive 16-column blocks (>= Kp * 16, padded)
+  int splits;      // split-K factor (1 = none)
+  float* partial;  // [splits][M][N] fp32 partial sums when splits > 1
+  void* out;       // EPI_STORE/_F32/_RESID: [M, N]; EPI_SWIGLU: [M, N/2]; EPI_QKV: queries [M, d_model]
   int ldo;
   const void* resid;  // EPI_RESID: [M, N] (may alias out)
   int ldr;
@@ -64,7 +67,7 @@ struct AttnArgs {
   const void* ring_v;
   const DevSeg* segs;
   const int32_t* tiles;  // [n_tiles][2]: (segment, first row in segment)
-  int n_heads, max_pos, ld;  // ld = H*hd
+  int n_heads, max_pos, ldq, ldo;  // row strides of q and o (>= H*hd)
   float scale_log2;          // log2(e) / sqrt(hd)
 };
 
@@ -75,8 +78,17 @@ hipError_t launch_rmsnorm(int dtype, const void* x, int ldx, const int32_t* rows
 hipError_t launch_embed(int dtype, const int32_t* ids, const void* table, int vocab, const void* embeds, void* out,
                         int M, int D, int32_t* err_count, hipStream_t s);
 hipError_t launch_argmax(const float* logits, int n_rows, int V, int32_t* tokens, hipStream_t s);
-hipError_t launch_copy_rows(int dtype, void* dst, const void* const* srcs /*device array of 3*/, const int32_t* map,
-                            int n_rows, int row_len, hipStream_t s);
+// Fragment-tiles N rows of K elements (padded to Kp, a multiple of 32) for the GEMM; srcs is a
+// device array of source pointers, map (device, optional) gives (source, row) per output row.
+hipError_t launch_frag_pack(int dtype, void* dst, long bstride, const void* const* srcs, const int32_t* map, int N,
+                            int K, int Kp, hipStream_t s);
+// Padding that keeps concurrently read rows and weight streams off power-of-two strides, so
+// they spread over the L2 and HBM channels instead of queueing on one: 128 bytes.
+constexpr int STRIDE_PAD_BYTES = 128;
+inline long frag_bstride(int Kp, int dtype) { return (long)Kp * 16 + STRIDE_PAD_BYTES / (dtype == AF_BF16 ? 2 : 4); }
+int gemm_block_m(int dtype, int M);  // rows per GEMM workgroup tile for M packed rows
+int gemm_block_n();                  // columns per GEMM workgroup tile
+int gemm_k_align();                  // K of the packed weights is a multiple of this
 
 constexpr int ATTN_BQ = 64;   // query rows per attention work tile
 constexpr int ATTN_BKV = 64;  // keys per LDS tile

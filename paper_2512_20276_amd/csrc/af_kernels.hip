@@ -9,15 +9,17 @@
 //   EPI_RESID   residual add in place (OutputProj and down projection);
 //   EPI_SWIGLU  SiLU(gate) * up;
 //   EPI_STORE*  plain store (bf16/fp32) and fp32 logits.
-// Pairs for the rotary and SwiGLU epilogues: the weights are repacked so that output
-// columns come in 16-column blocks [a-block, b-block]; with 16x16 accumulator tiles the
-// partner of an element sits in the same lane and register of the next block.
+// Pairs for the rotary and SwiGLU epilogues: the weights are repacked so that each 16-column
+// block holds 8 a-columns and then their 8 partners; in a 16x16 accumulator tile the partner
+// of lane l's element is lane l ^ 8's, one lane exchange away.
 //
 // Operand fragments: for both MFMAs a lane (r = lane % 16, g = lane / 16) supplies eight
 // consecutive k values, k = 8g .. 8g+7 of a 32-wide k step, for row r of A or column r of
 // B; the accumulator tile gives lane (c = lane % 16, g) rows 4g .. 4g+3 of column c.  The
 // contraction only needs A and B to use the same lane/element -> k assignment.
 #include <hip/hip_runtime.h>
+
+#include <type_traits>
 
 #include "af_internal.h"
 
@@ -28,6 +30,7 @@ typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef __attribute__((__vector_size__(8 * sizeof(float)))) float f32x8;
+typedef __attribute__((__vector_size__(4 * sizeof(unsigned)))) unsigned u32x4;  // raw 16 bytes
 
 __device__ __forceinline__ float to_f(bf16 x) { return (float)x; }
 __device__ __forceinline__ float to_f(float x) { return x; }
@@ -66,191 +69,298 @@ struct Chunk {
 
 __device__ __forceinline__ uint4 zero4() { return make_uint4(0, 0, 0, 0); }
 
+// Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E).  Register arrays indexed
+// by such constants are promoted to registers before any loop transformation runs.
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
 // ------------------------------------------------------------------ XCD-aware tile order
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).  Give each
 // XCD a contiguous run of logical tiles so the M tiles that share a weight panel run on one
 // XCD and the panel is fetched from HBM once.
+#ifndef AF_XCD_REMAP
+#define AF_XCD_REMAP 1
+#endif
 __device__ __forceinline__ int xcd_remap(int bid, int total) {
+  if (!AF_XCD_REMAP) return bid;
   const int q = total / 8, r = total % 8;
   const int x = bid % 8, j = bid / 8;
   return x * q + (x < r ? x : r) + j;
 }
 
 // ------------------------------------------------------------------ GEMM
-template <typename T, int BM, int BN, int WM, int WN, int EPI>
-__global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(GemmArgs a) {
-  constexpr int NT = WM * WN * 64;
-  constexpr int VEC = Chunk<T>::N;               // elements per 16-byte chunk
-  constexpr int BK = 128 / sizeof(T);            // 128 bytes of k per row per stage
-  constexpr int KSTEPS = BK / 32;                // 32-wide MFMA k steps per stage
-  constexpr int LDS_ROW = BK + VEC;              // padded row (elements)
-  constexpr int CPR = BK / VEC;                  // chunks per row per stage (= 8)
-  constexpr int WTM = BM / WM, WTN = BN / WN;    // wave tile
-  constexpr int FM = WTM / 16, FN = WTN / 16;
-  constexpr int A_IT = (BM * CPR + NT - 1) / NT;
-  constexpr int B_IT = (BN * CPR + NT - 1) / NT;
-  static_assert(WTM % 16 == 0 && WTN % 32 == 0, "wave tile: 16-row and 32-column multiples");
-  typedef typename Mma<T>::frag frag;
-
-  __shared__ __attribute__((aligned(16))) T As[2][BM * LDS_ROW];
-  __shared__ __attribute__((aligned(16))) T Bs[2][BN * LDS_ROW];
-
-  const int n_mt = (a.M + BM - 1) / BM, n_nt = (a.N + BN - 1) / BN;
-  const int tile = xcd_remap(blockIdx.x, n_mt * n_nt);
-  const int m0 = (tile % n_mt) * BM, n0 = (tile / n_mt) * BN;
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm0 = (wave / WN) * WTM, wn0 = (wave % WN) * WTN;
-  const int lr = lane & 15, lg = lane >> 4;
-
-  const T* __restrict__ A = (const T*)a.A;
-  const T* __restrict__ B = (const T*)a.B;
-  const int nk = (a.K + BK - 1) / BK;
-
-  uint4 ra[A_IT], rb[B_IT];
-  auto load_stage = [&](int kt) {
-    const int k0 = kt * BK;
-#pragma unroll
-    for (int it = 0; it < A_IT; ++it) {
-      const int ci = tid + it * NT;
-      const int row = ci / CPR, c = ci % CPR;
-      const int gm = m0 + row, gk = k0 + c * VEC;
-      ra[it] = (ci < BM * CPR && gm < a.M && gk < a.K) ? *(const uint4*)(A + (size_t)gm * a.lda + gk) : zero4();
-    }
-#pragma unroll
-    for (int it = 0; it < B_IT; ++it) {
-      const int ci = tid + it * NT;
-      const int row = ci / CPR, c = ci % CPR;
-      const int gn = n0 + row, gk = k0 + c * VEC;
-      rb[it] = (ci < BN * CPR && gn < a.N && gk < a.K) ? *(const uint4*)(B + (size_t)gn * a.ldb + gk) : zero4();
-    }
-  };
-  auto store_stage = [&](int buf) {
-#pragma unroll
-    for (int it = 0; it < A_IT; ++it) {
-      const int ci = tid + it * NT;
-      if (ci < BM * CPR) *(uint4*)(&As[buf][(ci / CPR) * LDS_ROW + (ci % CPR) * VEC]) = ra[it];
-    }
-#pragma unroll
-    for (int it = 0; it < B_IT; ++it) {
-      const int ci = tid + it * NT;
-      if (ci < BN * CPR) *(uint4*)(&Bs[buf][(ci / CPR) * LDS_ROW + (ci % CPR) * VEC]) = rb[it];
-    }
-  };
-
-  f32x4 acc[FM][FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  load_stage(0);
-  store_stage(0);
-  __syncthreads();
-
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) load_stage(kt + 1);
-#pragma unroll
-    for (int ks = 0; ks < KSTEPS; ++ks) {
-      frag fa[FM], fb[FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-        fa[i] = *(const frag*)(&As[buf][(wm0 + i * 16 + lr) * LDS_ROW + ks * 32 + lg * 8]);
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-        fb[j] = *(const frag*)(&Bs[buf][(wn0 + j * 16 + lr) * LDS_ROW + ks * 32 + lg * 8]);
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = Mma<T>::mma(fa[i], fb[j], acc[i][j]);
-    }
-    if (kt + 1 < nk) store_stage(buf ^ 1);
-    __syncthreads();
+// Weights are stored fragment-tiled: block (n_blk, k_step) of 16 output columns x 32 k is
+// 64 lanes x 8 elements, contiguous, in exactly the order the MFMA B operand wants it, so
+// each wave streams its weight fragments from HBM straight into registers (one coalesced
+// 1 KB load per block for bf16) through a ring PF k-steps deep.  The activations, shared by
+// the four waves of a workgroup, go through LDS in the same fragment order (conflict-free
+// 16-byte reads), double-buffered per 128-byte k stage.  A workgroup covers BM rows x
+// 4 * WTN columns; split-K workgroups write fp32 partial tiles that a second kernel sums in
+// split order (deterministic) before the epilogue.
+template <typename T, int EPI>
+__device__ __forceinline__ void epi_single(const GemmArgs& a, int m, int n, float v) {
+  if constexpr (EPI == EPI_STORE) {
+    ((T*)a.out)[(size_t)m * a.ldo + n] = from_f<T>(v);
+  } else if constexpr (EPI == EPI_STORE_F32) {
+    ((float*)a.out)[(size_t)m * a.ldo + n] = v;
+  } else {  // EPI_RESID (out may alias resid: each element is read and written by one thread)
+    const float r = to_f(((const T*)a.resid)[(size_t)m * a.ldr + n]);
+    ((T*)a.out)[(size_t)m * a.ldo + n] = from_f<T>(r + v);
   }
+}
 
-  // ---------------- epilogue: lane holds rows m0+wm0+16i+4lg+e of column n0+wn0+16j+lr
-#pragma unroll
-  for (int i = 0; i < FM; ++i) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int m = m0 + wm0 + i * 16 + lg * 4 + e;
-      if (m >= a.M) continue;
-      if constexpr (EPI == EPI_STORE || EPI == EPI_STORE_F32 || EPI == EPI_RESID) {
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          const int n = n0 + wn0 + j * 16 + lr;
-          if (n >= a.N) continue;
-          const float v = acc[i][j][e];
-          if constexpr (EPI == EPI_STORE) {
-            ((T*)a.out)[(size_t)m * a.ldo + n] = from_f<T>(v);
-          } else if constexpr (EPI == EPI_STORE_F32) {
-            ((float*)a.out)[(size_t)m * a.ldo + n] = v;
-          } else {
-            const float r = to_f(((const T*)a.resid)[(size_t)m * a.ldr + n]);
-            ((T*)a.out)[(size_t)m * a.ldo + n] = from_f<T>(r + v);
-          }
-        }
-      } else {
-        // paired epilogues: block j (even) holds the a-halves, block j+1 their partners
-#pragma unroll
-        for (int j = 0; j < FN; j += 2) {
-          const int c = n0 + wn0 + j * 16 + lr;  // column of the a-element, in an even 16-block
-          if (c >= a.N) continue;
-          const float va = acc[i][j][e], vb = acc[i][j + 1][e];
-          if constexpr (EPI == EPI_SWIGLU) {
-            const int f = (c >> 5) * 16 + (c & 15);
-            const float s = va / (1.0f + __expf(-va));
-            ((T*)a.out)[(size_t)m * a.ldo + f] = from_f<T>(s * vb);
-          } else {  // EPI_QKV
-            const int D = a.d_model, hd = a.head_dim, half = hd >> 1;
-            const int region = c / D, cr = c - region * D;
-            const int h = cr / hd, jj = cr - h * hd;
-            const int dj = (jj >> 5) * 16 + (jj & 15);  // dimension j < hd/2 of this pair
-            const int slot = a.row_sp[2 * m], pos = a.row_sp[2 * m + 1];
-            if (region == 2) {
-              T* dst = (T*)a.ring_v + (((size_t)slot * a.n_heads + h) * a.max_pos + pos) * hd;
-              dst[dj] = from_f<T>(va);
-              dst[dj + half] = from_f<T>(vb);
-            } else {
-              const float cs = a.rope_cs[((size_t)pos * half + dj) * 2];
-              const float sn = a.rope_cs[((size_t)pos * half + dj) * 2 + 1];
-              const float ra_ = va * cs - vb * sn, rb_ = vb * cs + va * sn;
-              T* dst = region == 0 ? (T*)a.out + (size_t)m * a.ldo + h * hd
-                                   : (T*)a.ring_k + (((size_t)slot * a.n_heads + h) * a.max_pos + pos) * hd;
-              dst[dj] = from_f<T>(ra_);
-              dst[dj + half] = from_f<T>(rb_);
-            }
-          }
-        }
-      }
+// Paired epilogues: each 16-column block holds 8 a-columns followed by their 8 partners
+// (weights repacked that way); c is the a-column, va/vb the pair.
+template <typename T, int EPI>
+__device__ __forceinline__ void epi_pair(const GemmArgs& a, int m, int c, float va, float vb) {
+  if constexpr (EPI == EPI_SWIGLU) {
+    const int f = (c >> 4) * 8 + (c & 7);
+    const float s = va / (1.0f + __expf(-va));
+    ((T*)a.out)[(size_t)m * a.ldo + f] = from_f<T>(s * vb);
+  } else {  // EPI_QKV
+    const int D = a.d_model, hd = a.head_dim, half = hd >> 1;
+    const int region = c / D, cr = c - region * D;
+    const int h = cr / hd, jj = cr - h * hd;
+    const int dj = (jj >> 4) * 8 + (jj & 7);  // rotary pair (dj, dj + hd/2)
+    const int slot = a.row_sp[2 * m], pos = a.row_sp[2 * m + 1];
+    if (region == 2) {
+      T* dst = (T*)a.ring_v + (((size_t)slot * a.n_heads + h) * a.max_pos + pos) * hd;
+      dst[dj] = from_f<T>(va);
+      dst[dj + half] = from_f<T>(vb);
+    } else {
+      const float cs = a.rope_cs[((size_t)pos * half + dj) * 2];
+      const float sn = a.rope_cs[((size_t)pos * half + dj) * 2 + 1];
+      const float ra = va * cs - vb * sn, rb = vb * cs + va * sn;
+      T* dst = region == 0 ? (T*)a.out + (size_t)m * a.ldo + h * hd
+                           : (T*)a.ring_k + (((size_t)slot * a.n_heads + h) * a.max_pos + pos) * hd;
+      dst[dj] = from_f<T>(ra);
+      dst[dj + half] = from_f<T>(rb);
     }
   }
 }
 
-template <typename T, int BM, int BN, int WM, int WN>
-static hipError_t gemm_dispatch_epi(int epi, const GemmArgs& a, hipStream_t s) {
-  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
-  dim3 grid(tiles), block(WM * WN * 64);
+// Tile configuration: BM rows (all packed rows for M <= 288) x four waves of WTN columns;
+// PF weight k steps in flight per wave; DA activation stages in flight; OCC workgroups per CU.
+template <int BM_, int WTN_, int PF_, int DA_, int OCC_>
+struct GemmCfg {
+  static constexpr int BM = BM_, WTN = WTN_, PF = PF_, DA = DA_, OCC = OCC_;
+};
+
+template <typename T, typename C, int EPI>
+__global__ __launch_bounds__(256, C::OCC) void gemm_kernel(GemmArgs a) {
+  constexpr int BM = C::BM, WTN = C::WTN, PF = C::PF, DA = C::DA;
+  constexpr int BN = 4 * WTN;                  // four waves side by side along N
+  constexpr int FM = BM / 16, NFB = WTN / 16;  // 16x16 blocks per wave
+  constexpr int KPS = sizeof(T) == 2 ? 2 : 1;  // 32-wide k steps per 128-byte stage
+  constexpr int VEC = 16 / (int)sizeof(T);     // elements per 16-byte chunk
+  constexpr int A_IT = BM * 8 / 256;           // 16-byte activation chunks per thread per stage
+  constexpr int UNR = PF / KPS;                // stages per unrolled block
+  static_assert(BM % 32 == 0 && WTN % 16 == 0 && UNR % 2 == 0 && UNR % DA == 0 && A_IT >= 1, "tile shape");
+    typedef typename Mma<T>::frag frag;
+
+  __shared__ __attribute__((aligned(16))) T As[2][FM * KPS * 64 * 8];
+
+  // Kp is a multiple of 32 * PF and every split is a whole number of PF k steps, so each
+  // unrolled block of UNR stages is complete and the loop body has no guards.  Loads that
+  // run past the split read clamped, valid addresses and are never consumed.
+  const int n_mt = (a.M + BM - 1) / BM, n_nt = (a.N + BN - 1) / BN, S = a.splits;
+  const int t = xcd_remap(blockIdx.x, n_mt * n_nt * S);
+  const int mt = t % n_mt, rest = t / n_mt;
+  const int sp = rest % S, nt = rest / S;
+  const int m0 = mt * BM, n0 = nt * BN;
+  const int ksteps = a.Kp >> 5;
+  const int per = ((ksteps + S - 1) / S + PF - 1) / PF * PF;
+  const int kb = min(ksteps, sp * per), ke = min(ksteps, kb + per);
+  const int n_st = (ke - kb) / KPS;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nb0 = (n0 + wave * WTN) >> 4;  // first 16-column block of this wave
+  const int n_blocks = a.N >> 4;
+  const T* __restrict__ A = (const T*)a.A;
+  const T* __restrict__ Bf = (const T*)a.B;
+
+  const T* brow[NFB];  // this lane's fragment stream of each of its column blocks
+  static_for<0, NFB>([&](auto n) {
+    brow[n] = Bf + (size_t)min(nb0 + (int)n, n_blocks - 1) * a.bstride + lane * 8;
+  });
+  frag bq[PF][NFB];
+  auto load_b = [&](auto slot, int ks) {
+    const size_t kc = (size_t)min(ks, ksteps - 1) * 512;
+    static_for<0, NFB>([&](auto n) { bq[slot][n] = *(const frag*)(brow[n] + kc); });
+  };
+
+  // Activation chunks of this thread: row r, 16-byte column kl of each 128-byte stage.  Loads
+  // are unconditional from clamped addresses: rows >= M only feed output rows that are never
+  // stored, and k >= K meets zero weights (the packed weights are zero-padded to Kp), so the
+  // clamped values, finite activations, contribute nothing.
+  const T* arow[A_IT];
+  int a_kl[A_IT], lds_off[A_IT];
+  static_for<0, A_IT>([&](auto it) {
+    const int ci = tid + it * 256;
+    const int r = ci >> 3, kl = (ci & 7) * VEC;
+    arow[it] = A + (size_t)min(m0 + r, a.M - 1) * a.lda;
+    a_kl[it] = kl;
+    lds_off[it] = ((((r >> 4) * KPS + (kl >> 5)) * 64) + (r & 15) + 16 * ((kl & 31) >> 3)) * 8 + (kl & 7);
+  });
+  u32x4 ra[DA][A_IT];
+  auto load_a = [&](auto slot, int st) {
+    const int k0 = (kb + st * KPS) * 32;
+    static_for<0, A_IT>([&](auto it) { ra[slot][it] = *(const u32x4*)(arow[it] + min(k0 + a_kl[it], a.K - VEC)); });
+  };
+  auto store_a = [&](auto slot, auto buf) {
+    static_for<0, A_IT>([&](auto it) { *(u32x4*)(&As[buf][lds_off[it]]) = ra[slot][it]; });
+  };
+
+  f32x4 acc[FM][NFB];
+  static_for<0, FM>([&](auto i) { static_for<0, NFB>([&](auto n) { acc[i][n] = f32x4{0.f, 0.f, 0.f, 0.f}; }); });
+
+  if (n_st > 0) {
+    load_a(std::integral_constant<int, 0>{}, 0);
+    static_for<0, PF>([&](auto p) { load_b(p, kb + p); });
+    static_for<1, DA>([&](auto u) { load_a(u, u); });
+    store_a(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{});
+  }
+  __syncthreads();
+
+  for (int st0 = 0; st0 < n_st; st0 += UNR) {
+    static_for<0, UNR>([&](auto u) {
+      constexpr int U = decltype(u)::value;
+      const int st = st0 + U;
+      constexpr int buf = U & 1;  // st0 is a multiple of UNR (even), so buffers and slots are static
+      static_for<0, KPS>([&](auto j) {
+        constexpr int slot = U * KPS + decltype(j)::value;
+        static_for<0, FM>([&](auto i) {
+          const frag af = *(const frag*)(&As[buf][((i * KPS + j) * 64 + lane) * 8]);
+          static_for<0, NFB>([&](auto n) { acc[i][n] = Mma<T>::mma(af, bq[slot][n], acc[i][n]); });
+        });
+        load_b(std::integral_constant<int, slot>{}, kb + st * KPS + decltype(j)::value + PF);  // refill
+      });
+      store_a(std::integral_constant<int, (U + 1) % DA>{}, std::integral_constant<int, buf ^ 1>{});  // stage st+1
+      load_a(std::integral_constant<int, U % DA>{}, st + DA);  // the slot stage st used
+      __syncthreads();
+    });
+  }
+
+  // ---------------- epilogue: lane holds rows m0+16i+4lg+e of column (nb0+n)*16+lr
+  const int lr = lane & 15, lg = lane >> 4;
+  static_for<0, FM>([&](auto i) {
+    static_for<0, 4>([&](auto e) {
+      const int m = m0 + i * 16 + lg * 4 + e;
+      const bool row_ok = m < a.M;
+      static_for<0, NFB>([&](auto n) {
+        const int c = (nb0 + n) * 16 + lr;
+        const float v = acc[i][n][decltype(e)::value];
+        if constexpr (EPI == EPI_SWIGLU || EPI == EPI_QKV) {
+          const float partner = __shfl_xor(v, 8);  // all lanes take part
+          if (S == 1 && row_ok && c < a.N && (lr & 8) == 0) epi_pair<T, EPI>(a, m, c, v, partner);
+        } else {
+          if (S == 1 && row_ok && c < a.N) epi_single<T, EPI>(a, m, c, v);
+        }
+        if (S > 1 && row_ok && c < a.N) a.partial[((size_t)sp * a.M + m) * a.N + c] = v;
+      });
+    });
+  });
+}
+
+// Sums the split-K partials in split order and applies the epilogue; one thread per output
+// element (or per rotary/SwiGLU pair).
+template <typename T, int EPI>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
+  constexpr bool paired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
+  const int per_row = paired ? a.N / 2 : a.N;
+  const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (size_t)a.M * per_row) return;
+  const int m = (int)(idx / per_row), p = (int)(idx % per_row);
+  const size_t plane = (size_t)a.M * a.N;
+  if constexpr (paired) {
+    const int c = (p >> 3) * 16 + (p & 7);
+    float va = 0.f, vb = 0.f;
+    for (int s = 0; s < a.splits; ++s) {
+      va += a.partial[s * plane + (size_t)m * a.N + c];
+      vb += a.partial[s * plane + (size_t)m * a.N + c + 8];
+    }
+    epi_pair<T, EPI>(a, m, c, va, vb);
+  } else {
+    float v = 0.f;
+    for (int s = 0; s < a.splits; ++s) v += a.partial[s * plane + (size_t)m * a.N + p];
+    epi_single<T, EPI>(a, m, p, v);
+  }
+}
+
+template <typename T, typename C>
+static hipError_t gemm_launch_cfg(int epi, const GemmArgs& a, hipStream_t s) {
+  const int tiles = ((a.M + C::BM - 1) / C::BM) * ((a.N + 4 * C::WTN - 1) / (4 * C::WTN)) * a.splits;
+  dim3 grid(tiles), block(256);
   switch (epi) {
-    case EPI_STORE: hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, EPI_STORE>), grid, block, 0, s, a); break;
-    case EPI_STORE_F32: hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, EPI_STORE_F32>), grid, block, 0, s, a); break;
-    case EPI_RESID: hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, EPI_RESID>), grid, block, 0, s, a); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, EPI_SWIGLU>), grid, block, 0, s, a); break;
-    case EPI_QKV: hipLaunchKernelGGL((gemm_kernel<T, BM, BN, WM, WN, EPI_QKV>), grid, block, 0, s, a); break;
+    case EPI_STORE: hipLaunchKernelGGL((gemm_kernel<T, C, EPI_STORE>), grid, block, 0, s, a); break;
+    case EPI_STORE_F32: hipLaunchKernelGGL((gemm_kernel<T, C, EPI_STORE_F32>), grid, block, 0, s, a); break;
+    case EPI_RESID: hipLaunchKernelGGL((gemm_kernel<T, C, EPI_RESID>), grid, block, 0, s, a); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_kernel<T, C, EPI_SWIGLU>), grid, block, 0, s, a); break;
+    case EPI_QKV: hipLaunchKernelGGL((gemm_kernel<T, C, EPI_QKV>), grid, block, 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
 template <typename T>
-static hipError_t gemm_dispatch(int epi, const GemmArgs& a, hipStream_t s) {
-  if (a.M <= 32) return gemm_dispatch_epi<T, 32, 128, 1, 4>(epi, a, s);
-  return gemm_dispatch_epi<T, 96, 128, 2, 2>(epi, a, s);
+static hipError_t reduce_launch(int epi, const GemmArgs& a, hipStream_t s) {
+  const bool paired = epi == EPI_SWIGLU || epi == EPI_QKV;
+  const size_t n = (size_t)a.M * (paired ? a.N / 2 : a.N);
+  dim3 grid((unsigned)((n + 255) / 256)), block(256);
+  switch (epi) {
+    case EPI_STORE: hipLaunchKernelGGL((splitk_reduce_kernel<T, EPI_STORE>), grid, block, 0, s, a); break;
+    case EPI_STORE_F32: hipLaunchKernelGGL((splitk_reduce_kernel<T, EPI_STORE_F32>), grid, block, 0, s, a); break;
+    case EPI_RESID: hipLaunchKernelGGL((splitk_reduce_kernel<T, EPI_RESID>), grid, block, 0, s, a); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((splitk_reduce_kernel<T, EPI_SWIGLU>), grid, block, 0, s, a); break;
+    case EPI_QKV: hipLaunchKernelGGL((splitk_reduce_kernel<T, EPI_QKV>), grid, block, 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
+
+// Tiles: BM rows x four waves of 32 columns, two workgroups per CU.  Weight fragments stream
+// through a per-wave register ring (8 k steps for bf16, 4 for fp32) and activation stages
+// through a 4-deep register ring into double-buffered LDS.
+typedef GemmCfg<32, 32, 8, 4, 2> CfgS;    // M <= 32: weight streaming (decode-only steps, LM head)
+typedef GemmCfg<96, 32, 8, 4, 2> CfgM;
+typedef GemmCfg<128, 32, 8, 4, 2> CfgL;
+typedef GemmCfg<32, 32, 4, 4, 2> CfgF32S;  // fp32 (tiny models)
+typedef GemmCfg<96, 32, 4, 4, 2> CfgF32M;
+typedef GemmCfg<128, 32, 4, 4, 2> CfgF32L;
+
+// 32 rows for decode-sized steps, else whichever of 96 and 128 pads M the least.
+static int bm_for(int /*dtype*/, int M) {
+  if (M <= 32) return 32;
+  return ((M + 95) / 96) * 96 < ((M + 127) / 128) * 128 ? 96 : 128;
+}
+
+template <typename T>
+static hipError_t gemm_dispatch(int epi, const GemmArgs& a, hipStream_t s) {
+  hipError_t e;
+  const int bm = bm_for(0, a.M);
+  if constexpr (sizeof(T) == 2) {
+    e = bm == 32 ? gemm_launch_cfg<T, CfgS>(epi, a, s)
+        : bm == 96 ? gemm_launch_cfg<T, CfgM>(epi, a, s) : gemm_launch_cfg<T, CfgL>(epi, a, s);
+  } else {
+    e = bm == 32 ? gemm_launch_cfg<T, CfgF32S>(epi, a, s)
+        : bm == 96 ? gemm_launch_cfg<T, CfgF32M>(epi, a, s) : gemm_launch_cfg<T, CfgF32L>(epi, a, s);
+  }
+  if (e != hipSuccess || a.splits <= 1) return e;
+  return reduce_launch<T>(epi, a, s);
+}
+
+int gemm_block_m(int dtype, int M) { return bm_for(dtype, M); }
+int gemm_block_n() { return 128; }
+int gemm_k_align() { return 256; }
 
 hipError_t launch_gemm(int dtype, int epi, const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  if (a.splits < 1 || (a.splits > 1 && !a.partial)) return hipErrorInvalidValue;
   return dtype == AF_BF16 ? gemm_dispatch<bf16>(epi, a, s) : gemm_dispatch<float>(epi, a, s);
 }
 
@@ -294,7 +404,7 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a) {
 
   frag qf[KST];
   {
-    const T* qrow = (const T*)a.q + (size_t)(sg.q_start + qi_c) * a.ld + h * HD;
+    const T* qrow = (const T*)a.q + (size_t)(sg.q_start + qi_c) * a.ldq + h * HD;
 #pragma unroll
     for (int s = 0; s < KST; ++s) qf[s] = *(const frag*)(qrow + s * 32 + lg * 8);
   }
@@ -395,7 +505,7 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a) {
   float l_tot = l_run + __shfl_xor(l_run, 16);
   l_tot += __shfl_xor(l_tot, 32);
   const float inv = 1.0f / l_tot;
-  T* orow = (T*)a.o + (size_t)(sg.q_start + qi) * a.ld + h * HD;
+  T* orow = (T*)a.o + (size_t)(sg.q_start + qi) * a.ldo + h * HD;
 #pragma unroll
   for (int d = 0; d < DB; ++d)
 #pragma unroll
@@ -515,26 +625,36 @@ hipError_t launch_argmax(const float* logits, int n_rows, int V, int32_t* tokens
 }
 
 // ------------------------------------------------------------------ weight repacking
-// dst row r <- srcs[map[2r]] row map[2r+1]; rows of row_len elements, row_len % (16/size) == 0.
+// dst: fragment-tiled [N/16][Kp/32][64 lanes][8] (see the GEMM); source row n is
+// srcs[map[2n]] row map[2n+1] (or src0 row n without a map), rows of K elements, k >= K zero.
 template <typename T>
-__global__ __launch_bounds__(256) void copy_rows_kernel(T* __restrict__ dst, const T* const* srcs,
-                                                        const int32_t* __restrict__ map, int row_len) {
-  const int r = blockIdx.x;
-  const T* src = srcs[map[2 * r]] + (size_t)map[2 * r + 1] * row_len;
-  T* d = dst + (size_t)r * row_len;
-  constexpr int VEC = Chunk<T>::N;
-  for (int c = threadIdx.x; c < row_len / VEC; c += 256) ((uint4*)d)[c] = ((const uint4*)src)[c];
+__global__ __launch_bounds__(256) void frag_pack_kernel(T* __restrict__ dst, long bstride, const T* const* srcs,
+                                                        const int32_t* __restrict__ map, int N, int K, int Kp) {
+  const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const int ksteps = Kp >> 5;
+  const size_t total = (size_t)(N >> 4) * ksteps * 64;
+  if (idx >= total) return;
+  const int lane = (int)(idx & 63);
+  const size_t blk = idx >> 6;
+  const int ks = (int)(blk % ksteps), nb = (int)(blk / ksteps);
+  const int n = nb * 16 + (lane & 15), k0 = ks * 32 + 8 * (lane >> 4);
+  const T* src = map ? srcs[map[2 * n]] + (size_t)map[2 * n + 1] * K : srcs[0] + (size_t)n * K;
+  T* d = dst + (size_t)nb * bstride + ((size_t)ks * 64 + lane) * 8;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) d[e] = k0 + e < K ? src[k0 + e] : from_f<T>(0.f);
 }
 
-hipError_t launch_copy_rows(int dtype, void* dst, const void* const* srcs, const int32_t* map, int n_rows,
-                            int row_len, hipStream_t s) {
-  if (n_rows <= 0) return hipSuccess;
+hipError_t launch_frag_pack(int dtype, void* dst, long bstride, const void* const* srcs, const int32_t* map, int N,
+                            int K, int Kp, hipStream_t s) {
+  if (N <= 0 || N % 16 || Kp % 32 || Kp < K || bstride < (long)Kp * 16) return hipErrorInvalidValue;
+  const size_t total = (size_t)(N / 16) * (Kp / 32) * 64;
+  dim3 grid((unsigned)((total + 255) / 256)), block(256);
   if (dtype == AF_BF16)
-    hipLaunchKernelGGL(copy_rows_kernel<bf16>, dim3(n_rows), dim3(256), 0, s, (bf16*)dst, (const bf16* const*)srcs,
-                       map, row_len);
+    hipLaunchKernelGGL(frag_pack_kernel<bf16>, grid, block, 0, s, (bf16*)dst, bstride, (const bf16* const*)srcs, map,
+                       N, K, Kp);
   else
-    hipLaunchKernelGGL(copy_rows_kernel<float>, dim3(n_rows), dim3(256), 0, s, (float*)dst,
-                       (const float* const*)srcs, map, row_len);
+    hipLaunchKernelGGL(frag_pack_kernel<float>, grid, block, 0, s, (float*)dst, bstride, (const float* const*)srcs,
+                       map, N, K, Kp);
   return hipGetLastError();
 }
 

@@ -15,14 +15,18 @@ using namespace af;
 
 namespace {
 
+// Projection weights are stored fragment-tiled for the GEMM (K padded to a multiple of 32).
 struct Layer {
   void* attn_norm = nullptr;
-  void* wqkv = nullptr;  // [3d, d], rows in rotary-pair block order
+  void* wqkv = nullptr;  // [3d, d]: q, k, v rows, each head in rotary-pair 16-row block order
   void* wo = nullptr;    // [d, d]
   void* mlp_norm = nullptr;
-  void* wgu = nullptr;   // [2 d_ff, d], gate/up rows in 16-row block pairs
+  void* wgu = nullptr;   // [2 d_ff, d]: gate/up rows in alternating 16-row blocks
   void* wdown = nullptr; // [d, d_ff]
 };
+
+// K of the fragment-tiled weights: padded so the GEMM's k loop has no partial unrolled block.
+inline int padk(int k) { return (k + gemm_k_align() - 1) / gemm_k_align() * gemm_k_align(); }
 
 struct StageBuf {  // pinned staging for one descriptor upload
   int32_t* host = nullptr;
@@ -52,16 +56,21 @@ struct af_weights {
 
   // scratch activations, grown on demand
   int ws_M = 0, ws_emit = 0;
+  int ldD = 0, ldF = 0;  // padded row strides of the scratch activations
   void *xn = nullptr, *q = nullptr, *attn = nullptr, *act = nullptr, *emit_norm = nullptr;
   float* logits_ws = nullptr;
   int32_t* tokens_ws = nullptr;
   int32_t* dev_err = nullptr;
+
+  float* partial = nullptr;  // split-K partial sums
+  size_t partial_cap = 0;    // floats
 
   int32_t* desc_dev = nullptr;
   size_t desc_cap = 0;
   StageBuf stage[4];
   int stage_next = 0;
 
+  uint32_t options = 0;
   uint32_t timing_mask = 0;
   std::vector<TimedLaunch> timed;
   std::vector<hipEvent_t> event_pool;
@@ -283,10 +292,10 @@ af_status ensure_workspace(af_weights* w, int M, int n_emit) {
     w->xn = w->q = w->attn = w->act = nullptr;
     w->ws_M = 0;
     const int cap = std::max(M, 64);
-    AF_TRY(dev_alloc(w, &w->xn, (size_t)cap * d.d_model * w->es));
-    AF_TRY(dev_alloc(w, &w->q, (size_t)cap * d.d_model * w->es));
-    AF_TRY(dev_alloc(w, &w->attn, (size_t)cap * d.d_model * w->es));
-    AF_TRY(dev_alloc(w, &w->act, (size_t)cap * d.d_ff * w->es));
+    AF_TRY(dev_alloc(w, &w->xn, (size_t)cap * w->ldD * w->es));
+    AF_TRY(dev_alloc(w, &w->q, (size_t)cap * w->ldD * w->es));
+    AF_TRY(dev_alloc(w, &w->attn, (size_t)cap * w->ldD * w->es));
+    AF_TRY(dev_alloc(w, &w->act, (size_t)cap * w->ldF * w->es));
     w->ws_M = cap;
   }
   if (n_emit > w->ws_emit) {
@@ -299,7 +308,7 @@ af_status ensure_workspace(af_weights* w, int M, int n_emit) {
     w->tokens_ws = nullptr;
     w->ws_emit = 0;
     const int cap = std::max(n_emit, 16);
-    AF_TRY(dev_alloc(w, &w->emit_norm, (size_t)cap * d.d_model * w->es));
+    AF_TRY(dev_alloc(w, &w->emit_norm, (size_t)cap * w->ldD * w->es));
     AF_TRY(dev_alloc(w, (void**)&w->logits_ws, (size_t)cap * d.vocab * 4));
     AF_TRY(dev_alloc(w, (void**)&w->tokens_ws, (size_t)cap * 4));
     w->ws_emit = cap;
@@ -385,25 +394,57 @@ DevTables dev_tables(const af_weights* w, const StepDesc& sd) {
   return t;
 }
 
-GemmArgs gemm_args(const void* A, int lda, const void* B, int ldb, int M, int N, int K, void* out, int ldo) {
+GemmArgs gemm_args(int dtype, const void* A, int lda, const void* B, int M, int N, int K, void* out, int ldo) {
   GemmArgs g;
   std::memset(&g, 0, sizeof(g));
   g.A = A;
   g.lda = lda;
   g.B = B;
-  g.ldb = ldb;
   g.M = M;
   g.N = N;
   g.K = K;
+  g.Kp = padk(K);
+  g.bstride = frag_bstride(g.Kp, dtype);
+  g.splits = 1;
   g.out = out;
   g.ldo = ldo;
   return g;
 }
 
-af_status step_qkv(af_weights* w, int l, const void* xn, int M, af_ring* ring, const DevTables& t, void* q_out,
-                   hipStream_t s) {
+// Split K only when the output tiles alone would leave most of the 256 CUs idle: then the
+// largest factor (<= 4) that keeps all workgroups in one round (one per CU), with at least
+// one unrolled block of k steps per split.
+int choose_splits(int dtype, int M, int N, int Kp) {
+  const int bm = gemm_block_m(dtype, M), bn = gemm_block_n();
+  const int tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+  if (tiles >= 160) return 1;
+  int S = std::max(1, std::min(4, 256 / tiles));
+  while (S > 1 && Kp / S < gemm_k_align()) --S;
+  return S;
+}
+
+af_status with_splits(af_weights* w, GemmArgs& g) {
+  if (!w || (w->options & AF_OPT_NO_SPLIT_K)) return AF_OK;
+  const int S = choose_splits(w->d.dtype, g.M, g.N, g.Kp);
+  if (S <= 1) return AF_OK;
+  const size_t need = (size_t)S * g.M * g.N;
+  if (need > w->partial_cap) {
+    AF_HIP(hipDeviceSynchronize());
+    dev_free(w, w->partial);
+    w->partial = nullptr;
+    w->partial_cap = 0;
+    AF_TRY(dev_alloc(w, (void**)&w->partial, need * 4));
+    w->partial_cap = need;
+  }
+  g.splits = S;
+  g.partial = w->partial;
+  return AF_OK;
+}
+
+af_status step_qkv(af_weights* w, int l, const void* xn, int ldx, int M, af_ring* ring, const DevTables& t,
+                   void* q_out, int ldq, hipStream_t s) {
   const af_model_desc& d = w->d;
-  GemmArgs g = gemm_args(xn, d.d_model, w->layers[l].wqkv, d.d_model, M, 3 * d.d_model, d.d_model, q_out, d.d_model);
+  GemmArgs g = gemm_args(d.dtype, xn, ldx, w->layers[l].wqkv, M, 3 * d.d_model, d.d_model, q_out, ldq);
   const size_t es = w->es;
   g.ring_k = (char*)ring->kv + ring->offset(l, 0, 0, 0, 0) * es;
   g.ring_v = (char*)ring->kv + ring->offset(l, 1, 0, 0, 0) * es;
@@ -413,11 +454,12 @@ af_status step_qkv(af_weights* w, int l, const void* xn, int M, af_ring* ring, c
   g.head_dim = d.head_dim;
   g.n_heads = d.n_heads;
   g.max_pos = ring->d.max_pos;
+  AF_TRY(with_splits(w, g));
   return timed(w, AF_K_GEMM_QKV, s, [&] { return launch_gemm(d.dtype, EPI_QKV, g, s); });
 }
 
-af_status step_attention(af_weights* w, int dtype, af_ring* ring, int l, const void* q, void* o, const DevTables& t,
-                         hipStream_t s) {
+af_status step_attention(af_weights* w, int dtype, af_ring* ring, int l, const void* q, int ldq, void* o, int ldo,
+                         const DevTables& t, hipStream_t s) {
   AttnArgs a;
   std::memset(&a, 0, sizeof(a));
   const size_t es = dtype_size(dtype);
@@ -429,51 +471,56 @@ af_status step_attention(af_weights* w, int dtype, af_ring* ring, int l, const v
   a.tiles = t.tiles;
   a.n_heads = ring->d.n_kv_heads;
   a.max_pos = ring->d.max_pos;
-  a.ld = ring->d.n_kv_heads * ring->d.head_dim;
+  a.ldq = ldq;
+  a.ldo = ldo;
   a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)ring->d.head_dim));
   return timed(w, AF_K_ATTENTION, s, [&] { return launch_attention(dtype, ring->d.head_dim, a, t.n_tiles, s); });
 }
 
-af_status step_o(af_weights* w, int l, const void* o, void* hidden, int M, hipStream_t s) {
+af_status step_o(af_weights* w, int l, const void* o, int ldo_in, void* hidden, int M, hipStream_t s) {
   const af_model_desc& d = w->d;
-  GemmArgs g = gemm_args(o, d.d_model, w->layers[l].wo, d.d_model, M, d.d_model, d.d_model, hidden, d.d_model);
+  GemmArgs g = gemm_args(d.dtype, o, ldo_in, w->layers[l].wo, M, d.d_model, d.d_model, hidden, d.d_model);
   g.resid = hidden;
   g.ldr = d.d_model;
+  AF_TRY(with_splits(w, g));
   return timed(w, AF_K_GEMM_O, s, [&] { return launch_gemm(d.dtype, EPI_RESID, g, s); });
 }
 
-af_status step_gate_up(af_weights* w, int l, const void* xn, void* act, int M, hipStream_t s) {
+af_status step_gate_up(af_weights* w, int l, const void* xn, int ldx, void* act, int ld_act, int M, hipStream_t s) {
   const af_model_desc& d = w->d;
-  GemmArgs g = gemm_args(xn, d.d_model, w->layers[l].wgu, d.d_model, M, 2 * d.d_ff, d.d_model, act, d.d_ff);
+  GemmArgs g = gemm_args(d.dtype, xn, ldx, w->layers[l].wgu, M, 2 * d.d_ff, d.d_model, act, ld_act);
+  AF_TRY(with_splits(w, g));
   return timed(w, AF_K_GEMM_GATEUP, s, [&] { return launch_gemm(d.dtype, EPI_SWIGLU, g, s); });
 }
 
-af_status step_down(af_weights* w, int l, const void* act, void* hidden, int M, hipStream_t s) {
+af_status step_down(af_weights* w, int l, const void* act, int ld_act, void* hidden, int M, hipStream_t s) {
   const af_model_desc& d = w->d;
-  GemmArgs g = gemm_args(act, d.d_ff, w->layers[l].wdown, d.d_ff, M, d.d_model, d.d_ff, hidden, d.d_model);
+  GemmArgs g = gemm_args(d.dtype, act, ld_act, w->layers[l].wdown, M, d.d_model, d.d_ff, hidden, d.d_model);
   g.resid = hidden;
   g.ldr = d.d_model;
+  AF_TRY(with_splits(w, g));
   return timed(w, AF_K_GEMM_DOWN, s, [&] { return launch_gemm(d.dtype, EPI_RESID, g, s); });
 }
 
-af_status step_norm(af_weights* w, const void* x, const int32_t* rows, const void* g, void* y, int n_rows,
-                    hipStream_t s) {
+af_status step_norm(af_weights* w, const void* x, int ldx, const int32_t* rows, const void* g, void* y, int ldy,
+                    int n_rows, hipStream_t s) {
   const af_model_desc& d = w->d;
   return timed(w, AF_K_RMSNORM, s, [&] {
-    return launch_rmsnorm(d.dtype, x, d.d_model, rows, g, y, d.d_model, n_rows, d.d_model, d.rms_eps, s);
+    return launch_rmsnorm(d.dtype, x, ldx, rows, g, y, ldy, n_rows, d.d_model, d.rms_eps, s);
   });
 }
 
 af_status layer_forward(af_weights* w, int l, void* hidden, int M, af_ring* ring, const DevTables& t, hipStream_t s) {
   const Layer& L = w->layers[l];
-  AF_TRY(step_norm(w, hidden, nullptr, L.attn_norm, w->xn, M, s));
-  AF_TRY(step_qkv(w, l, w->xn, M, ring, t, w->q, s));
-  AF_TRY(step_attention(w, w->d.dtype, ring, l, w->q, w->attn, t, s));
+  const int D = w->d.d_model, ldD = w->ldD, ldF = w->ldF;
+  AF_TRY(step_norm(w, hidden, D, nullptr, L.attn_norm, w->xn, ldD, M, s));
+  AF_TRY(step_qkv(w, l, w->xn, ldD, M, ring, t, w->q, ldD, s));
+  AF_TRY(step_attention(w, w->d.dtype, ring, l, w->q, ldD, w->attn, ldD, t, s));
   // InPlaceKVShift: no device work; the slot rotation lives in the ring bookkeeping.
-  AF_TRY(step_o(w, l, w->attn, hidden, M, s));
-  AF_TRY(step_norm(w, hidden, nullptr, L.mlp_norm, w->xn, M, s));
-  AF_TRY(step_gate_up(w, l, w->xn, w->act, M, s));
-  AF_TRY(step_down(w, l, w->act, hidden, M, s));
+  AF_TRY(step_o(w, l, w->attn, ldD, hidden, M, s));
+  AF_TRY(step_norm(w, hidden, D, nullptr, L.mlp_norm, w->xn, ldD, M, s));
+  AF_TRY(step_gate_up(w, l, w->xn, ldD, w->act, ldF, M, s));
+  AF_TRY(step_down(w, l, w->act, ldF, hidden, M, s));
   return AF_OK;
 }
 
@@ -481,9 +528,10 @@ af_status lm_head(af_weights* w, const void* hidden, const DevTables& t, float* 
                   hipStream_t s) {
   const af_model_desc& d = w->d;
   if (t.n_emit == 0 || (!out_logits && !out_tokens)) return AF_OK;
-  AF_TRY(step_norm(w, hidden, t.emit_rows, w->final_norm, w->emit_norm, t.n_emit, s));
+  AF_TRY(step_norm(w, hidden, d.d_model, t.emit_rows, w->final_norm, w->emit_norm, w->ldD, t.n_emit, s));
   float* logits = out_logits ? out_logits : w->logits_ws;
-  GemmArgs g = gemm_args(w->emit_norm, d.d_model, w->lm_head, d.d_model, t.n_emit, d.vocab, d.d_model, logits, d.vocab);
+  GemmArgs g = gemm_args(d.dtype, w->emit_norm, w->ldD, w->lm_head, t.n_emit, d.vocab, d.d_model, logits, d.vocab);
+  AF_TRY(with_splits(w, g));
   AF_TRY(timed(w, AF_K_LM_HEAD, s, [&] { return launch_gemm(d.dtype, EPI_STORE_F32, g, s); }));
   if (out_tokens)
     AF_TRY(timed(w, AF_K_ARGMAX, s, [&] { return launch_argmax(logits, t.n_emit, d.vocab, out_tokens, s); }));
@@ -550,6 +598,8 @@ extern "C" af_status af_weights_create(const af_model_desc* desc, const void* co
   }
   w->d = d;
   w->es = dtype_size(d.dtype);
+  w->ldD = d.d_model + STRIDE_PAD_BYTES / (int)w->es;
+  w->ldF = d.d_ff + STRIDE_PAD_BYTES / (int)w->es;
   hipStream_t s = (hipStream_t)hip_stream;
   const size_t es = w->es;
   const int D = d.d_model, F = d.d_ff, V = d.vocab, hd = d.head_dim;
@@ -565,62 +615,68 @@ extern "C" af_status af_weights_create(const af_model_desc* desc, const void* co
   af_status st;
   if ((st = copy_new(&w->embed, tensors[0], (size_t)V * D * es)) != AF_OK) return fail(st);
   if ((st = copy_new(&w->final_norm, tensors[1], (size_t)D * es)) != AF_OK) return fail(st);
-  if ((st = copy_new(&w->lm_head, tensors[2], (size_t)V * D * es)) != AF_OK) return fail(st);
 
-  // Row maps of the repacked projections (source tensor, source row) per destination row.
-  // QKV: for each of q, k, v and each head, 16-row blocks [dims 16p.., dims hd/2 + 16p..].
+  // Row maps of the fused projections (source tensor, source row) per output row.  Every
+  // 16-row block holds 8 a-rows and then their 8 partners, so the GEMM epilogue finds a
+  // partner one lane away.  QKV: for each of q, k, v and each head, block p holds dims
+  // [8p, 8p + 8) and [hd/2 + 8p, hd/2 + 8p + 8) (the rotary pairs).
   std::vector<int32_t> qkv_map((size_t)3 * D * 2), gu_map((size_t)2 * F * 2);
   for (int c = 0; c < 3 * D; ++c) {
     const int region = c / D, cr = c % D, h = cr / hd, jj = cr % hd;
-    const int dim = (jj >> 5) * 16 + (jj & 15) + ((jj & 16) ? hd / 2 : 0);
+    const int dim = (jj >> 4) * 8 + (jj & 7) + ((jj & 8) ? hd / 2 : 0);
     qkv_map[2 * c] = region;
     qkv_map[2 * c + 1] = h * hd + dim;
   }
-  // gate/up: 16-row blocks [gate rows 16p.., up rows 16p..].
+  // gate/up: block p holds gate rows [8p, 8p + 8) and up rows [8p, 8p + 8).
   for (int c = 0; c < 2 * F; ++c) {
-    gu_map[2 * c] = (c & 16) ? 1 : 0;
-    gu_map[2 * c + 1] = (c >> 5) * 16 + (c & 15);
+    gu_map[2 * c] = (c & 8) ? 1 : 0;
+    gu_map[2 * c + 1] = (c >> 4) * 8 + (c & 7);
   }
+  // device array of source pointers: per layer [wq, wk, wv, w_gate, w_up, wo, w_down, -], then lm_head
+  const size_t n_ptr = (size_t)d.n_layers * 8 + 8;
+  std::vector<const void*> srcs(n_ptr, nullptr);
+  for (int l = 0; l < d.n_layers; ++l) {
+    const void* const* t = tensors + 3 + 9 * l;
+    srcs[8 * l + 0] = t[1];
+    srcs[8 * l + 1] = t[2];
+    srcs[8 * l + 2] = t[3];
+    srcs[8 * l + 3] = t[6];
+    srcs[8 * l + 4] = t[7];
+    srcs[8 * l + 5] = t[4];
+    srcs[8 * l + 6] = t[8];
+  }
+  srcs[(size_t)d.n_layers * 8] = tensors[2];
   int32_t *qkv_map_d = nullptr, *gu_map_d = nullptr;
   const void** srcs_d = nullptr;
   if ((st = dev_alloc(w, (void**)&qkv_map_d, qkv_map.size() * 4)) != AF_OK) return fail(st);
   if ((st = dev_alloc(w, (void**)&gu_map_d, gu_map.size() * 4)) != AF_OK) return fail(st);
-  if ((st = dev_alloc(w, (void**)&srcs_d, (size_t)d.n_layers * 3 * 2 * sizeof(void*) + 64)) != AF_OK) return fail(st);
-  std::vector<const void*> srcs((size_t)d.n_layers * 6);
-  for (int l = 0; l < d.n_layers; ++l) {
-    const void* const* t = tensors + 3 + 9 * l;
-    srcs[6 * l + 0] = t[1];
-    srcs[6 * l + 1] = t[2];
-    srcs[6 * l + 2] = t[3];
-    srcs[6 * l + 3] = t[6];
-    srcs[6 * l + 4] = t[7];
-    srcs[6 * l + 5] = nullptr;
-  }
+  if ((st = dev_alloc(w, (void**)&srcs_d, n_ptr * sizeof(void*))) != AF_OK) return fail(st);
   hipError_t he = hipMemcpy(qkv_map_d, qkv_map.data(), qkv_map.size() * 4, hipMemcpyHostToDevice);
   if (he == hipSuccess) he = hipMemcpy(gu_map_d, gu_map.data(), gu_map.size() * 4, hipMemcpyHostToDevice);
-  if (he == hipSuccess && d.n_layers > 0)
-    he = hipMemcpy(srcs_d, srcs.data(), srcs.size() * sizeof(void*), hipMemcpyHostToDevice);
+  if (he == hipSuccess) he = hipMemcpy(srcs_d, srcs.data(), n_ptr * sizeof(void*), hipMemcpyHostToDevice);
   if (he != hipSuccess) {
     set_error("af_weights_create: map upload failed: %s", hipGetErrorString(he));
     return fail(AF_ERR_DEVICE);
   }
+  const int Dp = padk(D), Fp = padk(F);
+  auto pack = [&](void** dst, const void* const* src_d, const int32_t* map, int N, int K, int Kp) -> af_status {
+    const long bs = frag_bstride(Kp, d.dtype);
+    AF_TRY(dev_alloc(w, dst, (size_t)(N / 16) * bs * es));
+    AF_HIP(launch_frag_pack(d.dtype, *dst, bs, src_d, map, N, K, Kp, s));
+    return AF_OK;
+  };
+  if ((st = pack(&w->lm_head, srcs_d + (size_t)d.n_layers * 8, nullptr, V, D, Dp)) != AF_OK) return fail(st);
   w->layers.resize(d.n_layers);
   for (int l = 0; l < d.n_layers; ++l) {
     const void* const* t = tensors + 3 + 9 * l;
     Layer& L = w->layers[l];
+    const void* const* sl = srcs_d + 8 * (size_t)l;
     if ((st = copy_new(&L.attn_norm, t[0], (size_t)D * es)) != AF_OK) return fail(st);
-    if ((st = copy_new(&L.wo, t[4], (size_t)D * D * es)) != AF_OK) return fail(st);
     if ((st = copy_new(&L.mlp_norm, t[5], (size_t)D * es)) != AF_OK) return fail(st);
-    if ((st = copy_new(&L.wdown, t[8], (size_t)D * F * es)) != AF_OK) return fail(st);
-    if ((st = dev_alloc(w, &L.wqkv, (size_t)3 * D * D * es)) != AF_OK) return fail(st);
-    if ((st = dev_alloc(w, &L.wgu, (size_t)2 * F * D * es)) != AF_OK) return fail(st);
-    he = launch_copy_rows(d.dtype, L.wqkv, (const void* const*)(srcs_d + 6 * l), qkv_map_d, 3 * D, D, s);
-    if (he == hipSuccess)
-      he = launch_copy_rows(d.dtype, L.wgu, (const void* const*)(srcs_d + 6 * l + 3), gu_map_d, 2 * F, D, s);
-    if (he != hipSuccess) {
-      set_error("af_weights_create: repack launch failed: %s", hipGetErrorString(he));
-      return fail(AF_ERR_DEVICE);
-    }
+    if ((st = pack(&L.wqkv, sl, qkv_map_d, 3 * D, D, Dp)) != AF_OK) return fail(st);
+    if ((st = pack(&L.wgu, sl + 3, gu_map_d, 2 * F, D, Dp)) != AF_OK) return fail(st);
+    if ((st = pack(&L.wo, sl + 5, nullptr, D, D, Dp)) != AF_OK) return fail(st);
+    if ((st = pack(&L.wdown, sl + 6, nullptr, D, F, Fp)) != AF_OK) return fail(st);
   }
   if ((st = dev_alloc(w, (void**)&w->dev_err, 64)) != AF_OK) return fail(st);
   he = hipMemsetAsync(w->dev_err, 0, 64, s);
@@ -728,8 +784,27 @@ extern "C" af_status af_op_linear(int32_t dtype, const void* x, const void* wt, 
     set_error("af_op_linear: need K %% %d == 0 and N %% 16 == 0", vec);
     return AF_ERR_UNSUPPORTED;
   }
-  GemmArgs g = gemm_args(x, K, wt, K, M, N, K, y, N);
-  AF_HIP(launch_gemm(dtype, EPI_STORE, g, (hipStream_t)hip_stream));
+  // the caller's weight is row-major [N, K]: fragment-tile a private copy (synchronous)
+  hipStream_t s = (hipStream_t)hip_stream;
+  const int Kp = padk(K);
+  void* wf = nullptr;
+  const void** src_d = nullptr;
+  const long bs = frag_bstride(Kp, dtype);
+  AF_HIP(hipMalloc(&wf, (size_t)(N / 16) * bs * dtype_size(dtype)));
+  hipError_t e = hipMalloc((void**)&src_d, sizeof(void*));
+  if (e == hipSuccess) e = hipMemcpy(src_d, &wt, sizeof(void*), hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = launch_frag_pack(dtype, wf, bs, src_d, nullptr, N, K, Kp, s);
+  if (e == hipSuccess) {
+    GemmArgs g = gemm_args(dtype, x, K, wf, M, N, K, y, N);
+    e = launch_gemm(dtype, EPI_STORE, g, s);
+  }
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  (void)hipFree(wf);
+  if (src_d) (void)hipFree(src_d);
+  if (e != hipSuccess) {
+    set_error("af_op_linear: %s", hipGetErrorString(e));
+    return AF_ERR_DEVICE;
+  }
   return AF_OK;
 }
 
@@ -744,7 +819,7 @@ extern "C" af_status af_op_qkv_rope_write(af_weights* w, int32_t layer, const vo
   hipStream_t s = (hipStream_t)hip_stream;
   StepDesc sd;
   AF_TRY(prepare_step(w, ring, segs, n_seg, M, layer + 1, sd, s));
-  return step_qkv(w, layer, xn, M, ring, dev_tables(w, sd), q_out, s);
+  return step_qkv(w, layer, xn, w->d.d_model, M, ring, dev_tables(w, sd), q_out, w->d.d_model, s);
 }
 
 extern "C" af_status af_op_attention(af_ring* ring, int32_t layer, const void* q, int32_t M, const af_segment* segs,
@@ -771,7 +846,8 @@ extern "C" af_status af_op_attention(af_ring* ring, int32_t layer, const void* q
     t.emit_rows = dd + sd.off_emit;
     t.n_tiles = sd.n_tiles;
     t.n_emit = sd.n_emit;
-    st = step_attention(nullptr, ring->d.dtype, ring, layer, q, o, t, s);
+    const int ld = ring->d.n_kv_heads * ring->d.head_dim;
+    st = step_attention(nullptr, ring->d.dtype, ring, layer, q, ld, o, ld, t, s);
     if (st == AF_OK) e = hipStreamSynchronize(s);
   }
   (void)hipFree(dd);
@@ -789,7 +865,7 @@ extern "C" af_status af_op_o_proj_residual(af_weights* w, int32_t layer, const v
     set_error("af_op_o_proj_residual: bad argument");
     return AF_ERR_INVALID_ARG;
   }
-  return step_o(w, layer, o, hidden, M, (hipStream_t)hip_stream);
+  return step_o(w, layer, o, w->d.d_model, hidden, M, (hipStream_t)hip_stream);
 }
 
 extern "C" af_status af_op_gate_up_swiglu(af_weights* w, int32_t layer, const void* xn, void* act, int32_t M,
@@ -799,7 +875,7 @@ extern "C" af_status af_op_gate_up_swiglu(af_weights* w, int32_t layer, const vo
     set_error("af_op_gate_up_swiglu: bad argument");
     return AF_ERR_INVALID_ARG;
   }
-  return step_gate_up(w, layer, xn, act, M, (hipStream_t)hip_stream);
+  return step_gate_up(w, layer, xn, w->d.d_model, act, w->d.d_ff, M, (hipStream_t)hip_stream);
 }
 
 extern "C" af_status af_op_down_residual(af_weights* w, int32_t layer, const void* act, void* hidden, int32_t M,
@@ -809,7 +885,7 @@ extern "C" af_status af_op_down_residual(af_weights* w, int32_t layer, const voi
     set_error("af_op_down_residual: bad argument");
     return AF_ERR_INVALID_ARG;
   }
-  return step_down(w, layer, act, hidden, M, (hipStream_t)hip_stream);
+  return step_down(w, layer, act, w->d.d_ff, hidden, M, (hipStream_t)hip_stream);
 }
 
 extern "C" af_status af_op_lm_head_argmax(af_weights* w, const void* hidden, int32_t M, const af_segment* segs,
@@ -830,6 +906,16 @@ extern "C" af_status af_op_lm_head_argmax(af_weights* w, const void* hidden, int
   AF_TRY(ensure_workspace(w, M, sd.n_emit));
   AF_TRY(upload_desc(w, sd, s));
   return lm_head(w, hidden, dev_tables(w, sd), out_logits, out_tokens, s);
+}
+
+extern "C" af_status af_weights_set_options(af_weights* w, uint32_t flags) {
+  clear_error();
+  if (!w || (flags & ~AF_OPT_NO_SPLIT_K)) {
+    set_error("af_weights_set_options: bad argument");
+    return AF_ERR_INVALID_ARG;
+  }
+  w->options = flags;
+  return AF_OK;
 }
 
 // ================================================================ timing
