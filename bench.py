@@ -44,7 +44,103 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
     p.add_argument("--no-timing-pass", action="store_true")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="before warm-up, run one streaming copy of COPY_BYTES (read once, written once) "
+                        "whose hardware-counter readings scale the FETCH_SIZE / WRITE_SIZE of the others")
+    p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                   help="print the traffic summary of two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE "
+                        "counter_collection.csv files of a --copy-calibration run) and exit")
+    p.add_argument("--summarize-stats", metavar="KERNEL_STATS_CSV",
+                   help="print a per-kernel table of a rocprofv3 --kernel-trace --stats kernel_stats.csv and exit")
     return p.parse_args()
+
+
+COPY_BYTES = 1 << 30        # calibration copy: 1 GiB read + 1 GiB written, far beyond the 256 MB last-level cache
+KERNELS_SRC = os.path.join(ROOT, "paper_2512_20276_amd", "csrc", "af_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_gemm_gateup_7b_m282.md")
+
+
+def kernels_sha256():
+    import hashlib
+    with open(KERNELS_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per gate/up launch from the committed counter summary, or None when the kernel
+    source has changed since the counters were taken."""
+    try:
+        kv = dict(l.split(":", 1) for l in open(TRAFFIC_FILE).read().splitlines() if l.startswith("- ") and ":" in l)
+    except OSError:
+        return None
+    kv = {k[2:].strip(): v.strip().strip("`") for k, v in kv.items()}
+    if kv.get("kernel_source_sha256") != kernels_sha256():
+        return None
+    return int(kv["traffic_bytes_per_launch"])
+
+
+def _kernel_class(name: str) -> str:
+    """Maps a demangled kernel name to the label used in the summaries."""
+    import re
+    if "gemm_kernel" in name:
+        epi = (re.search(r",\s*(\d)>\s*\(", name) or re.search(r",\s*\(af::Epi\)(\d)>", name)
+               or re.search(r"GemmCfgI(?:Li\d+E)+EELi(\d)E", name))   # demangled or mangled
+        e = int(epi.group(1)) if epi else -1
+        return {0: "gemm (store)", 1: "gemm (f32 store, LM head)", 2: "gemm (+residual: O / down)",
+                3: "gemm (gate/up + SwiGLU)", 4: "gemm (QKV + RoPE + ring write)"}.get(e, "gemm")
+    for key in ("splitk_reduce", "attention_kernel", "rmsnorm_kernel", "embed_kernel", "argmax_kernel",
+                "frag_pack_kernel"):
+        if key in name:
+            return key
+    if "neg" in name.lower():
+        return "calibration copy (torch.neg, out=)"
+    return name[:60]
+
+
+def summarize_stats(path):
+    import csv
+    rows = list(csv.DictReader(open(path)))
+    print("| kernel | calls | avg us | min us | max us | total ms | % |")
+    print("|---|---:|---:|---:|---:|---:|---:|")
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        print(f"| `{_kernel_class(r['Name'])}`: `{r['Name'][:100]}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+              f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
+              f"{float(r['TotalDurationNs']) / 1e6:.3f} | {float(r['Percentage']):.2f} |")
+
+
+def summarize_pmc(fetch_csv, write_csv):
+    """Average FETCH_SIZE / WRITE_SIZE (KiB per dispatch) per kernel class, scaled by the readings
+    of the calibration copy, which fetches and writes COPY_BYTES."""
+    import csv
+    from collections import defaultdict
+
+    def per_class(path, counter):
+        acc = defaultdict(lambda: [0.0, 0])
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            a = acc[_kernel_class(r["Kernel_Name"])]
+            a[0] += float(r["Counter_Value"])
+            a[1] += 1
+        return {k: (v / n, n) for k, (v, n) in acc.items()}
+
+    f, w = per_class(fetch_csv, "FETCH_SIZE"), per_class(write_csv, "WRITE_SIZE")
+    cal = "calibration copy (torch.neg, out=)"
+    fs = COPY_BYTES / (f[cal][0] * 1024)
+    ws = COPY_BYTES / (w[cal][0] * 1024)
+    print(f"calibration: copy of {COPY_BYTES} B reads FETCH_SIZE {f[cal][0]:.0f} KiB, WRITE_SIZE {w[cal][0]:.0f} KiB "
+          f"-> scale fetch x{fs:.4f}, write x{ws:.4f}\n")
+    print("| kernel class | dispatches | FETCH KiB/dispatch | WRITE KiB/dispatch | HBM bytes/dispatch (scaled) |")
+    print("|---|---:|---:|---:|---:|")
+    for k in sorted(f, key=lambda k: -f[k][0] * f[k][1]):
+        wk = w.get(k, (0.0, 0))[0]
+        tb = f[k][0] * 1024 * fs + wk * 1024 * ws
+        print(f"| {k} | {f[k][1]} | {f[k][0]:.0f} | {wk:.0f} | {tb:.4g} |")
+    g = "gemm (gate/up + SwiGLU)"
+    if g in f:
+        tb = int(round(f[g][0] * 1024 * fs + w[g][0] * 1024 * ws))
+        print(f"\n- traffic_bytes_per_launch: {tb}")
+        print(f"- kernel_source_sha256: `{kernels_sha256()}`")
 
 
 # ----------------------------------------------------------------------------- algorithmic work
@@ -122,6 +218,12 @@ def cpu_baseline(seconds_budget: float):
 # ----------------------------------------------------------------------------- main
 def main():
     args = parse()
+    if args.summarize_stats:
+        summarize_stats(args.summarize_stats)
+        return
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (each MI355X would run its "
               "own independent pipelines); run with --gpus 1", file=sys.stderr)
@@ -158,6 +260,14 @@ def main():
         pool.append(e)
     pipe = Pipeline(w, ring, K, pids, lambda t: pool[t % len(pool)], keep_history=False)
     torch.cuda.synchronize()
+    if args.copy_calibration:
+        src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.neg(src, out=dst)   # one elementwise pass: every byte read once and written once
+        torch.cuda.synchronize()
+        del src, dst
+        torch.cuda.empty_cache()
     log(f"setup {time.time() - t0:.1f} s; warm-up {args.warmup} steps")
 
     for _ in range(args.warmup):
@@ -211,7 +321,7 @@ def main():
         at_gbs = at_bytes / (at_ms / at_n * 1e-3) / 1e9
         out["roofline"] = {"kernel": "gemm_kernel, SwiGLU epilogue (gate/up projection)",
                            "bound": "hbm", "achieved": round(ga_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                           "frac": round(ga_gbs / PEAK_HBM_GBS, 4), "traffic": None,
+                           "frac": round(ga_gbs / PEAK_HBM_GBS, 4), "traffic": measured_traffic(),
                            "bytes_per_launch": ga_bytes, "avg_launch_us": round(ga_avg * 1e3, 2),
                            "tflops": round(ga_flops / (ga_avg * 1e-3) / 1e12, 1)}
         out["mfma_frac_projection_gemms"] = round(mfma_frac, 4)
