@@ -42,14 +42,20 @@ struct DevSeg {            // 8 x int32
 enum Epi { EPI_STORE = 0, EPI_STORE_F32 = 1, EPI_RESID = 2, EPI_SWIGLU = 3, EPI_QKV = 4 };
 
 struct GemmArgs {
-  const void* A;  // [M, K] activations, row stride lda elements
-  const void* B;  // weights, fragment-tiled: n-block nb at B + nb * bstride, [Kp/32][64][8] each
+  // Activations [M, K]: row-major with row stride lda (fp32), or fragment-tiled (bf16) when
+  // astride > 0: 32-row block b at A + b * astride, laid out as frag_off() gives.
+  const void* A;
+  // Weights, fragment-tiled per column block: bf16 blocks of 32 columns x 16 k (the B operand
+  // of the 32x32x16 MFMA), fp32 blocks of 16 columns x 32 k; block nb at B + nb * bstride.
+  const void* B;
   int M, N, K, Kp, lda;
-  long bstride;    // elements between consecutive 16-column blocks (>= Kp * 16, padded)
+  long astride;
+  long bstride;
   int splits;      // split-K factor (1 = none)
   float* partial;  // [splits][M][N] fp32 partial sums when splits > 1
   void* out;       // EPI_STORE/_F32/_RESID: [M, N]; EPI_SWIGLU: [M, N/2]; EPI_QKV: queries [M, d_model]
   int ldo;
+  long ostride;    // EPI_SWIGLU: > 0 writes the output fragment-tiled (32-row blocks ostride apart)
   const void* resid;  // EPI_RESID: [M, N] (may alias out)
   int ldr;
   // EPI_QKV
@@ -68,13 +74,19 @@ struct AttnArgs {
   const DevSeg* segs;
   const int32_t* tiles;  // [n_tiles][2]: (segment, first row in segment)
   int n_heads, max_pos, ldq, ldo;  // row strides of q and o (>= H*hd)
+  long ostride;              // > 0: o is written fragment-tiled (32-row blocks ostride apart)
   float scale_log2;          // log2(e) / sqrt(hd)
 };
 
 hipError_t launch_gemm(int dtype, int epi, const GemmArgs& a, hipStream_t s);
 hipError_t launch_attention(int dtype, int head_dim, const AttnArgs& a, int n_tiles, hipStream_t s);
+// y row-major (row stride ldy) or, when ystride > 0, fragment-tiled.
 hipError_t launch_rmsnorm(int dtype, const void* x, int ldx, const int32_t* rows, const void* g, void* y, int ldy,
-                          int n_rows, int D, float eps, hipStream_t s);
+                          long ystride, int n_rows, int D, float eps, hipStream_t s);
+// Row-major [M, K] (row stride ld) -> fragment-tiled (32-row blocks astride apart), with the
+// rows of the last block past M and the columns [K, Kp) written as zeros.
+hipError_t launch_to_frag(int dtype, const void* x, int ld, int M, int K, int Kp, void* y, long astride,
+                          hipStream_t s);
 hipError_t launch_embed(int dtype, const int32_t* ids, const void* table, int vocab, const void* embeds, void* out,
                         int M, int D, int32_t* err_count, hipStream_t s);
 hipError_t launch_argmax(const float* logits, int n_rows, int V, int32_t* tokens, hipStream_t s);
@@ -85,9 +97,18 @@ hipError_t launch_frag_pack(int dtype, void* dst, long bstride, const void* cons
 // Padding that keeps concurrently read rows and weight streams off power-of-two strides, so
 // they spread over the L2 and HBM channels instead of queueing on one: 128 bytes.
 constexpr int STRIDE_PAD_BYTES = 128;
-inline long frag_bstride(int Kp, int dtype) { return (long)Kp * 16 + STRIDE_PAD_BYTES / (dtype == AF_BF16 ? 2 : 4); }
-int gemm_block_m(int dtype, int M);  // rows per GEMM workgroup tile for M packed rows
-int gemm_block_n();                  // columns per GEMM workgroup tile
+// Columns per packed weight block: 32 for bf16 (32x32x16 MFMA), 16 for fp32 (16x16x4 MFMA).
+inline int frag_ncols(int dtype) { return dtype == AF_BF16 ? 32 : 16; }
+inline long frag_bstride(int Kp, int dtype) {
+  return (long)Kp * frag_ncols(dtype) + STRIDE_PAD_BYTES / (dtype == AF_BF16 ? 2 : 4);
+}
+// Fragment-tiled activations: one 32-row block holds [Kp/16][64 lanes][8]; lane = row % 32 +
+// 32 * ((k % 16) / 8), element k % 8.  Blocks are astride elements apart.
+inline long frag_astride(int Kp) { return (long)Kp * 32 + STRIDE_PAD_BYTES / 2; }
+__host__ __device__ inline size_t frag_off(int m, int k, long astride) {
+  return (size_t)(m >> 5) * astride + (size_t)(k >> 4) * 512 + (size_t)(((m & 31) + ((k >> 3) & 1) * 32) * 8 + (k & 7));
+}
+int gemm_splits(int dtype, int M, int N, int Kp);  // split-K factor that fills the GPU
 int gemm_k_align();                  // K of the packed weights is a multiple of this
 
 constexpr int ATTN_BQ = 64;   // query rows per attention work tile

@@ -1,24 +1,21 @@
 // gfx950 kernels of the Cross-Request State Packed Forward.
 //
 // Every projection is an NT GEMM C[m][n] = sum_k A[m][k] * B[n][k] with A the packed
-// activations (M = prefill + decode rows) and B a weight matrix in [out, in] layout, on
-// 16x16 MFMA tiles (v_mfma_f32_16x16x32_bf16 for bf16; eight v_mfma_f32_16x16x4f32 for
-// fp32), fp32 accumulation, with the step that follows it fused into the epilogue:
+// activations (M = prefill + decode rows) and B a weight matrix in [out, in] layout, with fp32
+// accumulation and the step that follows it fused into the epilogue:
 //   EPI_QKV     rotary embedding at each row's own position, queries to a buffer, keys and
 //               values straight into the row's ring slot (Alg. 2 FusedRoPEAndWriteKV);
 //   EPI_RESID   residual add in place (OutputProj and down projection);
 //   EPI_SWIGLU  SiLU(gate) * up;
 //   EPI_STORE*  plain store (bf16/fp32) and fp32 logits.
+// bf16 runs on v_mfma_f32_32x32x16_bf16 (gemm32_kernel) with both operands fragment-tiled in
+// HBM; fp32 (small models) on v_mfma_f32_16x16x4f32 with row-major activations (gemm_kernel).
 // Pairs for the rotary and SwiGLU epilogues: the weights are repacked so that each 16-column
-// block holds 8 a-columns and then their 8 partners; in a 16x16 accumulator tile the partner
+// group holds 8 a-columns and then their 8 partners; in either accumulator layout the partner
 // of lane l's element is lane l ^ 8's, one lane exchange away.
-//
-// Operand fragments: for both MFMAs a lane (r = lane % 16, g = lane / 16) supplies eight
-// consecutive k values, k = 8g .. 8g+7 of a 32-wide k step, for row r of A or column r of
-// B; the accumulator tile gives lane (c = lane % 16, g) rows 4g .. 4g+3 of column c.  The
-// contraction only needs A and B to use the same lane/element -> k assignment.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "af_internal.h"
@@ -30,6 +27,7 @@ typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef __attribute__((__vector_size__(8 * sizeof(float)))) float f32x8;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 typedef __attribute__((__vector_size__(4 * sizeof(unsigned)))) unsigned u32x4;  // raw 16 bytes
 
 __device__ __forceinline__ float to_f(bf16 x) { return (float)x; }
@@ -121,7 +119,8 @@ __device__ __forceinline__ void epi_pair(const GemmArgs& a, int m, int c, float 
   if constexpr (EPI == EPI_SWIGLU) {
     const int f = (c >> 4) * 8 + (c & 7);
     const float s = va / (1.0f + __expf(-va));
-    ((T*)a.out)[(size_t)m * a.ldo + f] = from_f<T>(s * vb);
+    const size_t o = a.ostride > 0 ? frag_off(m, f, a.ostride) : (size_t)m * a.ldo + f;
+    ((T*)a.out)[o] = from_f<T>(s * vb);
   } else {  // EPI_QKV
     const int D = a.d_model, hd = a.head_dim, half = hd >> 1;
     const int region = c / D, cr = c - region * D;
@@ -323,45 +322,209 @@ static hipError_t reduce_launch(int epi, const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Tiles: BM rows x four waves of 32 columns, two workgroups per CU.  Weight fragments stream
-// through a per-wave register ring (8 k steps for bf16, 4 for fp32) and activation stages
-// through a 4-deep register ring into double-buffered LDS.
-typedef GemmCfg<32, 32, 8, 4, 2> CfgS;    // M <= 32: weight streaming (decode-only steps, LM head)
-typedef GemmCfg<96, 32, 8, 4, 2> CfgM;
-typedef GemmCfg<128, 32, 8, 4, 2> CfgL;
-typedef GemmCfg<32, 32, 4, 4, 2> CfgF32S;  // fp32 (tiny models)
+// fp32 tiles (small models): BM rows x four waves of 32 columns, two workgroups per CU; weight
+// fragments stream through a per-wave register ring 4 k steps deep, activations through a
+// 4-deep register ring into double-buffered LDS.
+typedef GemmCfg<32, 32, 4, 4, 2> CfgF32S;
 typedef GemmCfg<96, 32, 4, 4, 2> CfgF32M;
 typedef GemmCfg<128, 32, 4, 4, 2> CfgF32L;
 
 // 32 rows for decode-sized steps, else whichever of 96 and 128 pads M the least.
-static int bm_for(int /*dtype*/, int M) {
+static int bm_for_f32(int M) {
   if (M <= 32) return 32;
   return ((M + 95) / 96) * 96 < ((M + 127) / 128) * 128 ? 96 : 128;
 }
 
-template <typename T>
-static hipError_t gemm_dispatch(int epi, const GemmArgs& a, hipStream_t s) {
-  hipError_t e;
-  const int bm = bm_for(0, a.M);
-  if constexpr (sizeof(T) == 2) {
-    e = bm == 32 ? gemm_launch_cfg<T, CfgS>(epi, a, s)
-        : bm == 96 ? gemm_launch_cfg<T, CfgM>(epi, a, s) : gemm_launch_cfg<T, CfgL>(epi, a, s);
-  } else {
-    e = bm == 32 ? gemm_launch_cfg<T, CfgF32S>(epi, a, s)
-        : bm == 96 ? gemm_launch_cfg<T, CfgF32M>(epi, a, s) : gemm_launch_cfg<T, CfgF32L>(epi, a, s);
-  }
+static hipError_t gemm_dispatch_f32(int epi, const GemmArgs& a, hipStream_t s) {
+  const int bm = bm_for_f32(a.M);
+  hipError_t e = bm == 32 ? gemm_launch_cfg<float, CfgF32S>(epi, a, s)
+                 : bm == 96 ? gemm_launch_cfg<float, CfgF32M>(epi, a, s) : gemm_launch_cfg<float, CfgF32L>(epi, a, s);
   if (e != hipSuccess || a.splits <= 1) return e;
-  return reduce_launch<T>(epi, a, s);
+  return reduce_launch<float>(epi, a, s);
 }
 
-int gemm_block_m(int dtype, int M) { return bm_for(dtype, M); }
-int gemm_block_n() { return 128; }
+// ------------------------------------------------------------------ bf16 GEMM (32x32x16 MFMA)
+// A workgroup is four waves side by side along N (32 columns each: a 128-column tile) over FM
+// 32-row blocks (all packed rows up to 32 * FM) and one K split.  K advances in stages of
+// four 16-wide k steps.
+//  - Activations: a stage is FM x 4 fragment blocks of 1 KB, copied L2 -> LDS by
+//    global_load_lds (each wave issues FM of them), with NBUF = 4 stages in flight; every wave
+//    reads all of them from LDS, so each activation byte crosses L2 -> CU once per tile.
+//  - Weights: each wave streams its own 32-column block into an 8-slot register ring two
+//    stages ahead.  These loads are written as inline asm: the compiler would otherwise sink
+//    them next to their use or drain them with waits of its own; the one vmcnt wait per stage
+//    (issued with the barrier) covers them, and the ring's slots are fixed per unrolled stage.
+//  - Per stage a wave waits and meets the barrier, issues the DMAs of stage st + 3, then runs
+//    4 k steps of FM MFMAs with the next step's LDS reads issued ahead, refilling one weight
+//    slot per step.
+// Splits cover whole units of 4 stages (K is padded to a multiple of 256).
+template <int FM, int EPI>
+__global__ __launch_bounds__(256, 1) void gemm32_kernel(GemmArgs a) {
+  constexpr int NW = 4, KS = 4, NBUF = 4, PFB = 8, BLK = 512;
+  constexpr int SB = FM * KS;  // fragment blocks per stage
+  constexpr int D = SB / NW;   // DMAs per wave per stage
+  constexpr int P = PFB / KS;  // stages of weight lookahead
+  static_assert(SB % NW == 0 && (NBUF * KS) % PFB == 0 && P >= 1 && P <= NBUF - 1, "pipeline shape");
+  __shared__ __attribute__((aligned(1024))) bf16 As[NBUF][SB * BLK];
+
+  const int tid = threadIdx.x, lane = tid & 63, nw = tid >> 6;
+  const int n_blocks = (a.N + 31) >> 5, n_nt = (n_blocks + NW - 1) / NW;
+  const int m_blocks = (a.M + 31) >> 5, n_mt = (m_blocks + FM - 1) / FM;
+  const int S = a.splits;
+  const int t = xcd_remap(blockIdx.x, n_mt * n_nt * S);
+  const int mt = t % n_mt, rest = t / n_mt;
+  const int sp = rest % S, nt = rest / S;
+  const int ks16 = a.Kp >> 4;
+  const int units = ks16 / (KS * NBUF), per = (units + S - 1) / S;
+  const int kb = min(units, sp * per) * (KS * NBUF), ke = min(units, sp * per + per) * (KS * NBUF);
+  const int n_st = (ke - kb) / KS;  // a multiple of NBUF
+  const int nb_raw = nt * NW + nw;
+  const int nb = min(nb_raw, n_blocks - 1);  // a wave past N streams a valid block and stores nothing
+
+  const bf16* __restrict__ Ab = (const bf16*)a.A;
+  const bf16* bp = (const bf16*)a.B + (size_t)nb * a.bstride + lane * 8;
+  bf16x8 rb[PFB];
+  auto load_b = [&](auto slot, int st, int j) {
+    const int k = min(kb + st * KS + j, ks16 - 1);
+    const bf16* src = bp + (size_t)k * BLK;
+    bf16x8 v;
+    asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(src) : "memory");
+    rb[slot] = v;
+  };
+  // stage st's block q (m-block q / KS of the tile, k step q % KS) lands at As[buf][q * BLK]
+  auto dma = [&](auto buf, int st) {
+    static_for<0, D>([&](auto d) {
+      const int q = nw + NW * decltype(d)::value, mb = q / KS, j = q % KS;
+      const int k = min(kb + st * KS + j, ks16 - 1);
+      const int blk = min(mt * FM + mb, m_blocks - 1);  // rows past M: a valid block, never stored
+      const bf16* src = Ab + (size_t)blk * a.astride + (size_t)k * BLK + lane * 8;
+      __builtin_amdgcn_global_load_lds((const void*)src, (__attribute__((address_space(3))) void*)&As[buf][q * BLK],
+                                       16, 0, 0);
+    });
+  };
+
+  f32x16 acc[FM];
+  static_for<0, FM>([&](auto i) { acc[i] = f32x16{}; });
+  static_for<0, NBUF - 1>([&](auto b) {
+    dma(b, b);
+    __builtin_amdgcn_sched_barrier(0);
+  });
+  static_for<0, P>([&](auto s) {
+    static_for<0, KS>([&](auto j) { load_b(std::integral_constant<int, s * KS + j>{}, s, j); });
+  });
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the loop's waits count from a full ring
+  __builtin_amdgcn_sched_barrier(0);
+
+  for (int st0 = 0; st0 < n_st; st0 += NBUF) {
+    static_for<0, NBUF>([&](auto u) {
+      constexpr int U = decltype(u)::value;
+      const int st = st0 + U;
+      // Stage st's weights (the last loads of stage st - P) and activations (DMA'd NBUF - 1
+      // stages back, earlier still) must have landed, in every wave (the barrier also frees
+      // buffer (st - 1) % NBUF for the next DMA).  Loads issued after stage st's last weight
+      // load: P - 1 stages of D DMAs + KS weight loads.
+      constexpr int WAIT = (P - 1) * (D + KS);
+      asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(WAIT) : "memory");
+      dma(std::integral_constant<int, (U + NBUF - 1) % NBUF>{}, st + NBUF - 1);
+      __builtin_amdgcn_sched_barrier(0);
+      bf16x8 af[2][FM];
+      static_for<0, FM>([&](auto i) { af[0][i] = *(const bf16x8*)(&As[U][(i * KS) * BLK + lane * 8]); });
+      static_for<0, KS>([&](auto j) {
+        constexpr int J = decltype(j)::value;
+        constexpr int slot = (U * KS + J) % PFB;
+        if constexpr (J + 1 < KS) {
+          static_for<0, FM>([&](auto i) {
+            af[(J + 1) & 1][i] = *(const bf16x8*)(&As[U][(i * KS + J + 1) * BLK + lane * 8]);
+          });
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        static_for<0, FM>([&](auto i) {
+          acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[J & 1][i], rb[slot], acc[i], 0, 0, 0);
+        });
+        load_b(std::integral_constant<int, slot>{}, st + P, J);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    });
+  }
+  // The ring's last (unused) loads land before any of its registers can be reused.
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int p = 0; p < PFB; ++p) asm volatile("" : "+v"(rb[p]));
+
+  // ---------------- epilogue: acc[i][r] is row 32 (mt FM + i) + 8 (r / 4) + 4 (lane / 32) + r % 4
+  // of column 32 nb + lane % 32
+  const int nc = nb_raw * 32 + (lane & 31);
+  const bool col_ok = nb_raw < n_blocks && nc < a.N;
+  static_for<0, FM>([&](auto i) {
+    static_for<0, 16>([&](auto r) {
+      constexpr int R = decltype(r)::value;
+      const int m = (mt * FM + (int)decltype(i)::value) * 32 + 8 * (R / 4) + 4 * (lane >> 5) + (R % 4);
+      const float v = acc[i][R];
+      const bool ok = col_ok && m < a.M;
+      if constexpr (EPI == EPI_SWIGLU || EPI == EPI_QKV) {
+        const float partner = __shfl_xor(v, 8);  // all lanes take part
+        if (S == 1 && ok && (lane & 8) == 0) epi_pair<bf16, EPI>(a, m, nc, v, partner);
+      } else {
+        if (S == 1 && ok) epi_single<bf16, EPI>(a, m, nc, v);
+      }
+      if (S > 1 && ok) a.partial[((size_t)sp * a.M + m) * a.N + nc] = v;
+    });
+  });
+}
+
+static int fm_for(int M) {
+  const int mb = (M + 31) / 32;
+  return mb <= 1 ? 1 : mb <= 3 ? 3 : 9;
+}
+
+template <int FM>
+static hipError_t gemm32_launch(int epi, const GemmArgs& a, hipStream_t s) {
+  const int n_nt = ((a.N + 31) / 32 + 3) / 4, n_mt = ((a.M + 31) / 32 + FM - 1) / FM;
+  dim3 grid(n_mt * n_nt * a.splits), block(256);
+  switch (epi) {
+    case EPI_STORE: hipLaunchKernelGGL((gemm32_kernel<FM, EPI_STORE>), grid, block, 0, s, a); break;
+    case EPI_STORE_F32: hipLaunchKernelGGL((gemm32_kernel<FM, EPI_STORE_F32>), grid, block, 0, s, a); break;
+    case EPI_RESID: hipLaunchKernelGGL((gemm32_kernel<FM, EPI_RESID>), grid, block, 0, s, a); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm32_kernel<FM, EPI_SWIGLU>), grid, block, 0, s, a); break;
+    case EPI_QKV: hipLaunchKernelGGL((gemm32_kernel<FM, EPI_QKV>), grid, block, 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+static hipError_t gemm_dispatch_bf16(int epi, const GemmArgs& a, hipStream_t s) {
+  if (a.astride <= 0 || a.Kp % 256 != 0 || a.astride < (long)a.Kp * 32 || a.bstride < (long)a.Kp * 32)
+    return hipErrorInvalidValue;
+  const int fm = fm_for(a.M);
+  hipError_t e = fm == 1 ? gemm32_launch<1>(epi, a, s) : fm == 3 ? gemm32_launch<3>(epi, a, s) : gemm32_launch<9>(epi, a, s);
+  if (e != hipSuccess || a.splits <= 1) return e;
+  return reduce_launch<bf16>(epi, a, s);
+}
+
+// Split K only when the output tiles alone would leave most of the 256 CUs idle: then the
+// largest factor (<= 8 for bf16, 4 for fp32) that keeps all workgroups in one round, with at
+// least one whole unit of k steps per split.
+int gemm_splits(int dtype, int M, int N, int Kp) {
+  int tiles, cap;
+  if (dtype == AF_BF16) {
+    const int fm = fm_for(M);
+    tiles = (((M + 31) / 32 + fm - 1) / fm) * (((N + 31) / 32 + 3) / 4);
+    cap = 8;
+  } else {
+    const int bm = bm_for_f32(M);
+    tiles = ((M + bm - 1) / bm) * ((N + 127) / 128);
+    cap = 4;
+  }
+  if (tiles >= 160) return 1;
+  return std::max(1, std::min(std::min(cap, 256 / tiles), Kp / gemm_k_align()));
+}
+
 int gemm_k_align() { return 256; }
 
 hipError_t launch_gemm(int dtype, int epi, const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   if (a.splits < 1 || (a.splits > 1 && !a.partial)) return hipErrorInvalidValue;
-  return dtype == AF_BF16 ? gemm_dispatch<bf16>(epi, a, s) : gemm_dispatch<float>(epi, a, s);
+  return dtype == AF_BF16 ? gemm_dispatch_bf16(epi, a, s) : gemm_dispatch_f32(epi, a, s);
 }
 
 // ------------------------------------------------------------------ segment-aware attention
@@ -505,11 +668,21 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a) {
   float l_tot = l_run + __shfl_xor(l_run, 16);
   l_tot += __shfl_xor(l_tot, 32);
   const float inv = 1.0f / l_tot;
-  T* orow = (T*)a.o + (size_t)(sg.q_start + qi) * a.ldo + h * HD;
+  const int m = sg.q_start + qi;
+  if (a.ostride > 0) {  // fragment-tiled for the output projection: 4 consecutive k are contiguous
 #pragma unroll
-  for (int d = 0; d < DB; ++d)
+    for (int d = 0; d < DB; ++d) {
+      T* dst = (T*)a.o + frag_off(m, h * HD + d * 16 + lg * 4, a.ostride);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) orow[d * 16 + lg * 4 + e] = from_f<T>(oacc[d][e] * inv);
+      for (int e = 0; e < 4; ++e) dst[e] = from_f<T>(oacc[d][e] * inv);
+    }
+  } else {
+    T* orow = (T*)a.o + (size_t)m * a.ldo + h * HD;
+#pragma unroll
+    for (int d = 0; d < DB; ++d)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) orow[d * 16 + lg * 4 + e] = from_f<T>(oacc[d][e] * inv);
+  }
 }
 
 hipError_t launch_attention(int dtype, int head_dim, const AttnArgs& a, int n_tiles, hipStream_t s) {
@@ -528,19 +701,32 @@ hipError_t launch_attention(int dtype, int head_dim, const AttnArgs& a, int n_ti
 }
 
 // ------------------------------------------------------------------ RMSNorm
-// One workgroup of 256 threads per output row; rows[] optionally selects the input row.
+// One workgroup of 256 threads per output row; rows[] optionally selects the input row.  The
+// output is row-major (row stride ldy) or, with ystride > 0, fragment-tiled for the GEMM that
+// consumes it.  bf16 rows with D % 8 == 0 move 16 bytes per thread access.
 template <typename T>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const T* __restrict__ x, int ldx, const int32_t* rows,
-                                                      const T* __restrict__ g, T* __restrict__ y, int ldy, int D,
-                                                      float eps) {
+                                                      const T* __restrict__ g, T* __restrict__ y, int ldy,
+                                                      long ystride, int D, float eps) {
   __shared__ float red[4];
   const int r_out = blockIdx.x;
   const int r_in = rows ? rows[r_out] : r_out;
   const T* xr = x + (size_t)r_in * ldx;
+  constexpr int V = 16 / sizeof(T);
+  const bool vec = sizeof(T) == 2 && D % 8 == 0 && ldx % 8 == 0;
   float ss = 0.f;
-  for (int i = threadIdx.x; i < D; i += 256) {
-    const float v = to_f(xr[i]);
-    ss += v * v;
+  if (vec) {
+    for (int i = threadIdx.x * V; i < D; i += 256 * V) {
+      T v[V];
+      *(uint4*)v = *(const uint4*)(xr + i);
+#pragma unroll
+      for (int e = 0; e < V; ++e) ss += to_f(v[e]) * to_f(v[e]);
+    }
+  } else {
+    for (int i = threadIdx.x; i < D; i += 256) {
+      const float v = to_f(xr[i]);
+      ss += v * v;
+    }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
@@ -548,19 +734,56 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const T* __restrict__ x, i
   __syncthreads();
   const float tot = red[0] + red[1] + red[2] + red[3];
   const float inv = 1.0f / sqrtf(tot / (float)D + eps);
-  T* yr = y + (size_t)r_out * ldy;
-  for (int i = threadIdx.x; i < D; i += 256) yr[i] = from_f<T>(to_f(xr[i]) * inv * to_f(g[i]));
+  if (vec) {
+    for (int i = threadIdx.x * V; i < D; i += 256 * V) {
+      T v[V], gv[V], o[V];
+      *(uint4*)v = *(const uint4*)(xr + i);
+      *(uint4*)gv = *(const uint4*)(g + i);
+#pragma unroll
+      for (int e = 0; e < V; ++e) o[e] = from_f<T>(to_f(v[e]) * inv * to_f(gv[e]));
+      T* dst = ystride > 0 ? y + frag_off(r_out, i, ystride) : y + (size_t)r_out * ldy + i;
+      *(uint4*)dst = *(const uint4*)o;
+    }
+  } else {
+    for (int i = threadIdx.x; i < D; i += 256) {
+      const T o = from_f<T>(to_f(xr[i]) * inv * to_f(g[i]));
+      y[ystride > 0 ? frag_off(r_out, i, ystride) : (size_t)r_out * ldy + i] = o;
+    }
+  }
 }
 
 hipError_t launch_rmsnorm(int dtype, const void* x, int ldx, const int32_t* rows, const void* g, void* y, int ldy,
-                          int n_rows, int D, float eps, hipStream_t s) {
+                          long ystride, int n_rows, int D, float eps, hipStream_t s) {
   if (n_rows <= 0) return hipSuccess;
   if (dtype == AF_BF16)
     hipLaunchKernelGGL(rmsnorm_kernel<bf16>, dim3(n_rows), dim3(256), 0, s, (const bf16*)x, ldx, rows,
-                       (const bf16*)g, (bf16*)y, ldy, D, eps);
+                       (const bf16*)g, (bf16*)y, ldy, ystride, D, eps);
   else
     hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(n_rows), dim3(256), 0, s, (const float*)x, ldx, rows,
-                       (const float*)g, (float*)y, ldy, D, eps);
+                       (const float*)g, (float*)y, ldy, ystride, D, eps);
+  return hipGetLastError();
+}
+
+// Row-major -> fragment-tiled copy; one thread per 8 consecutive k of one row.
+__global__ __launch_bounds__(256) void to_frag_kernel(const bf16* __restrict__ x, int ld, int M, int K, int Kp,
+                                                      bf16* __restrict__ y, long astride, int rows_padded) {
+  const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const int groups = Kp / 8;
+  if (idx >= (size_t)rows_padded * groups) return;
+  const int m = (int)(idx / groups), k0 = (int)(idx % groups) * 8;
+  bf16 v[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = (m < M && k0 + e < K) ? x[(size_t)m * ld + k0 + e] : (bf16)0.f;
+  *(uint4*)(y + frag_off(m, k0, astride)) = *(const uint4*)v;
+}
+
+hipError_t launch_to_frag(int dtype, const void* x, int ld, int M, int K, int Kp, void* y, long astride,
+                          hipStream_t s) {
+  if (dtype != AF_BF16 || M <= 0 || K <= 0 || Kp < K || Kp % 16 || astride < (long)Kp * 32) return hipErrorInvalidValue;
+  const int rows_padded = (M + 31) / 32 * 32;
+  const size_t n = (size_t)rows_padded * (Kp / 8);
+  hipLaunchKernelGGL(to_frag_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, (const bf16*)x, ld, M, K, Kp,
+                     (bf16*)y, astride, rows_padded);
   return hipGetLastError();
 }
 
@@ -627,34 +850,45 @@ hipError_t launch_argmax(const float* logits, int n_rows, int V, int32_t* tokens
 // ------------------------------------------------------------------ weight repacking
 // dst: fragment-tiled [N/16][Kp/32][64 lanes][8] (see the GEMM); source row n is
 // srcs[map[2n]] row map[2n+1] (or src0 row n without a map), rows of K elements, k >= K zero.
-template <typename T>
+// Weight packing.  bf16: block (nb, k16) of 32 columns x 16 k, lane l -> column 32 nb + l % 32,
+// k = 16 k16 + 8 (l / 32) + e (the B operand of the 32x32x16 MFMA).  fp32: block (nb, k32) of 16
+// columns x 32 k, lane l -> column 16 nb + l % 16, k = 32 k32 + 8 (l / 16) + e.  Columns >= N
+// and k >= K are zero.
+template <typename T, int NC>
 __global__ __launch_bounds__(256) void frag_pack_kernel(T* __restrict__ dst, long bstride, const T* const* srcs,
                                                         const int32_t* __restrict__ map, int N, int K, int Kp) {
+  constexpr int KB = 512 / NC;  // k per block
   const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
-  const int ksteps = Kp >> 5;
-  const size_t total = (size_t)(N >> 4) * ksteps * 64;
+  const int ksteps = Kp / KB, n_blocks = (N + NC - 1) / NC;
+  const size_t total = (size_t)n_blocks * ksteps * 64;
   if (idx >= total) return;
   const int lane = (int)(idx & 63);
   const size_t blk = idx >> 6;
   const int ks = (int)(blk % ksteps), nb = (int)(blk / ksteps);
-  const int n = nb * 16 + (lane & 15), k0 = ks * 32 + 8 * (lane >> 4);
-  const T* src = map ? srcs[map[2 * n]] + (size_t)map[2 * n + 1] * K : srcs[0] + (size_t)n * K;
+  const int n = nb * NC + lane % NC, k0 = ks * KB + 8 * (lane / NC);
   T* d = dst + (size_t)nb * bstride + ((size_t)ks * 64 + lane) * 8;
+  if (n >= N) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) d[e] = from_f<T>(0.f);
+    return;
+  }
+  const T* src = map ? srcs[map[2 * n]] + (size_t)map[2 * n + 1] * K : srcs[0] + (size_t)n * K;
 #pragma unroll
   for (int e = 0; e < 8; ++e) d[e] = k0 + e < K ? src[k0 + e] : from_f<T>(0.f);
 }
 
 hipError_t launch_frag_pack(int dtype, void* dst, long bstride, const void* const* srcs, const int32_t* map, int N,
                             int K, int Kp, hipStream_t s) {
-  if (N <= 0 || N % 16 || Kp % 32 || Kp < K || bstride < (long)Kp * 16) return hipErrorInvalidValue;
-  const size_t total = (size_t)(N / 16) * (Kp / 32) * 64;
+  const int nc = frag_ncols(dtype);
+  if (N <= 0 || N % 16 || Kp % 32 || Kp < K || bstride < (long)Kp * nc) return hipErrorInvalidValue;
+  const size_t total = (size_t)((N + nc - 1) / nc) * (Kp * nc / 512) * 64;
   dim3 grid((unsigned)((total + 255) / 256)), block(256);
   if (dtype == AF_BF16)
-    hipLaunchKernelGGL(frag_pack_kernel<bf16>, grid, block, 0, s, (bf16*)dst, bstride, (const bf16* const*)srcs, map,
-                       N, K, Kp);
+    hipLaunchKernelGGL((frag_pack_kernel<bf16, 32>), grid, block, 0, s, (bf16*)dst, bstride,
+                       (const bf16* const*)srcs, map, N, K, Kp);
   else
-    hipLaunchKernelGGL(frag_pack_kernel<float>, grid, block, 0, s, (float*)dst, bstride, (const float* const*)srcs,
-                       map, N, K, Kp);
+    hipLaunchKernelGGL((frag_pack_kernel<float, 16>), grid, block, 0, s, (float*)dst, bstride,
+                       (const float* const*)srcs, map, N, K, Kp);
   return hipGetLastError();
 }
 

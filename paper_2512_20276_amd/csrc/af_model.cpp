@@ -54,9 +54,12 @@ struct af_weights {
   float* rope_cs = nullptr;  // [rope_cap][hd/2][2]
   int rope_cap = 0;
 
-  // scratch activations, grown on demand
+  // scratch activations, grown on demand.  bf16: the GEMM inputs xn, attn, act and emit_norm are
+  // fragment-tiled (32-row blocks xs_D / xs_F elements apart, zero-filled once so the K padding
+  // stays zero); fp32: row-major with the padded strides ldD / ldF.  q is row-major in both.
   int ws_M = 0, ws_emit = 0;
-  int ldD = 0, ldF = 0;  // padded row strides of the scratch activations
+  int ldD = 0, ldF = 0;
+  long xs_D = 0, xs_F = 0;
   void *xn = nullptr, *q = nullptr, *attn = nullptr, *act = nullptr, *emit_norm = nullptr;
   float* logits_ws = nullptr;
   int32_t* tokens_ws = nullptr;
@@ -281,6 +284,18 @@ af_status upload_desc(af_weights* w, const StepDesc& sd, hipStream_t s) {
   return AF_OK;
 }
 
+// Bytes of a GEMM-input activation buffer for `rows` rows of width K (layout per dtype).
+size_t act_bytes(const af_weights* w, int rows, bool wide) {
+  if (w->d.dtype == AF_BF16) return (size_t)((rows + 31) / 32) * (wide ? w->xs_F : w->xs_D) * w->es;
+  return (size_t)rows * (wide ? w->ldF : w->ldD) * w->es;
+}
+
+af_status alloc_zeroed(af_weights* w, void** p, size_t bytes) {
+  AF_TRY(dev_alloc(w, p, bytes));
+  AF_HIP(hipMemset(*p, 0, bytes));
+  return AF_OK;
+}
+
 af_status ensure_workspace(af_weights* w, int M, int n_emit) {
   const af_model_desc& d = w->d;
   if (M > w->ws_M) {
@@ -292,10 +307,10 @@ af_status ensure_workspace(af_weights* w, int M, int n_emit) {
     w->xn = w->q = w->attn = w->act = nullptr;
     w->ws_M = 0;
     const int cap = std::max(M, 64);
-    AF_TRY(dev_alloc(w, &w->xn, (size_t)cap * w->ldD * w->es));
+    AF_TRY(alloc_zeroed(w, &w->xn, act_bytes(w, cap, false)));
     AF_TRY(dev_alloc(w, &w->q, (size_t)cap * w->ldD * w->es));
-    AF_TRY(dev_alloc(w, &w->attn, (size_t)cap * w->ldD * w->es));
-    AF_TRY(dev_alloc(w, &w->act, (size_t)cap * w->ldF * w->es));
+    AF_TRY(alloc_zeroed(w, &w->attn, act_bytes(w, cap, false)));
+    AF_TRY(alloc_zeroed(w, &w->act, act_bytes(w, cap, true)));
     w->ws_M = cap;
   }
   if (n_emit > w->ws_emit) {
@@ -308,7 +323,7 @@ af_status ensure_workspace(af_weights* w, int M, int n_emit) {
     w->tokens_ws = nullptr;
     w->ws_emit = 0;
     const int cap = std::max(n_emit, 16);
-    AF_TRY(dev_alloc(w, &w->emit_norm, (size_t)cap * w->ldD * w->es));
+    AF_TRY(alloc_zeroed(w, &w->emit_norm, act_bytes(w, cap, false)));
     AF_TRY(dev_alloc(w, (void**)&w->logits_ws, (size_t)cap * d.vocab * 4));
     AF_TRY(dev_alloc(w, (void**)&w->tokens_ws, (size_t)cap * 4));
     w->ws_emit = cap;
@@ -394,11 +409,14 @@ DevTables dev_tables(const af_weights* w, const StepDesc& sd) {
   return t;
 }
 
-GemmArgs gemm_args(int dtype, const void* A, int lda, const void* B, int M, int N, int K, void* out, int ldo) {
+// A is row-major with stride lda (fp32) or fragment-tiled with block stride astride (bf16).
+GemmArgs gemm_args(int dtype, const void* A, int lda, long astride, const void* B, int M, int N, int K, void* out,
+                   int ldo) {
   GemmArgs g;
   std::memset(&g, 0, sizeof(g));
   g.A = A;
   g.lda = lda;
+  g.astride = astride;
   g.B = B;
   g.M = M;
   g.N = N;
@@ -411,21 +429,9 @@ GemmArgs gemm_args(int dtype, const void* A, int lda, const void* B, int M, int 
   return g;
 }
 
-// Split K only when the output tiles alone would leave most of the 256 CUs idle: then the
-// largest factor (<= 4) that keeps all workgroups in one round (one per CU), with at least
-// one unrolled block of k steps per split.
-int choose_splits(int dtype, int M, int N, int Kp) {
-  const int bm = gemm_block_m(dtype, M), bn = gemm_block_n();
-  const int tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
-  if (tiles >= 160) return 1;
-  int S = std::max(1, std::min(4, 256 / tiles));
-  while (S > 1 && Kp / S < gemm_k_align()) --S;
-  return S;
-}
-
 af_status with_splits(af_weights* w, GemmArgs& g) {
   if (!w || (w->options & AF_OPT_NO_SPLIT_K)) return AF_OK;
-  const int S = choose_splits(w->d.dtype, g.M, g.N, g.Kp);
+  const int S = gemm_splits(w->d.dtype, g.M, g.N, g.Kp);
   if (S <= 1) return AF_OK;
   const size_t need = (size_t)S * g.M * g.N;
   if (need > w->partial_cap) {
@@ -441,10 +447,10 @@ af_status with_splits(af_weights* w, GemmArgs& g) {
   return AF_OK;
 }
 
-af_status step_qkv(af_weights* w, int l, const void* xn, int ldx, int M, af_ring* ring, const DevTables& t,
+af_status step_qkv(af_weights* w, int l, const void* xn, int ldx, long xs, int M, af_ring* ring, const DevTables& t,
                    void* q_out, int ldq, hipStream_t s) {
   const af_model_desc& d = w->d;
-  GemmArgs g = gemm_args(d.dtype, xn, ldx, w->layers[l].wqkv, M, 3 * d.d_model, d.d_model, q_out, ldq);
+  GemmArgs g = gemm_args(d.dtype, xn, ldx, xs, w->layers[l].wqkv, M, 3 * d.d_model, d.d_model, q_out, ldq);
   const size_t es = w->es;
   g.ring_k = (char*)ring->kv + ring->offset(l, 0, 0, 0, 0) * es;
   g.ring_v = (char*)ring->kv + ring->offset(l, 1, 0, 0, 0) * es;
@@ -459,7 +465,7 @@ af_status step_qkv(af_weights* w, int l, const void* xn, int ldx, int M, af_ring
 }
 
 af_status step_attention(af_weights* w, int dtype, af_ring* ring, int l, const void* q, int ldq, void* o, int ldo,
-                         const DevTables& t, hipStream_t s) {
+                         long os, const DevTables& t, hipStream_t s) {
   AttnArgs a;
   std::memset(&a, 0, sizeof(a));
   const size_t es = dtype_size(dtype);
@@ -473,29 +479,32 @@ af_status step_attention(af_weights* w, int dtype, af_ring* ring, int l, const v
   a.max_pos = ring->d.max_pos;
   a.ldq = ldq;
   a.ldo = ldo;
+  a.ostride = os;
   a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)ring->d.head_dim));
   return timed(w, AF_K_ATTENTION, s, [&] { return launch_attention(dtype, ring->d.head_dim, a, t.n_tiles, s); });
 }
 
-af_status step_o(af_weights* w, int l, const void* o, int ldo_in, void* hidden, int M, hipStream_t s) {
+af_status step_o(af_weights* w, int l, const void* o, int ldo_in, long os, void* hidden, int M, hipStream_t s) {
   const af_model_desc& d = w->d;
-  GemmArgs g = gemm_args(d.dtype, o, ldo_in, w->layers[l].wo, M, d.d_model, d.d_model, hidden, d.d_model);
+  GemmArgs g = gemm_args(d.dtype, o, ldo_in, os, w->layers[l].wo, M, d.d_model, d.d_model, hidden, d.d_model);
   g.resid = hidden;
   g.ldr = d.d_model;
   AF_TRY(with_splits(w, g));
   return timed(w, AF_K_GEMM_O, s, [&] { return launch_gemm(d.dtype, EPI_RESID, g, s); });
 }
 
-af_status step_gate_up(af_weights* w, int l, const void* xn, int ldx, void* act, int ld_act, int M, hipStream_t s) {
+af_status step_gate_up(af_weights* w, int l, const void* xn, int ldx, long xs, void* act, int ld_act, long act_os,
+                       int M, hipStream_t s) {
   const af_model_desc& d = w->d;
-  GemmArgs g = gemm_args(d.dtype, xn, ldx, w->layers[l].wgu, M, 2 * d.d_ff, d.d_model, act, ld_act);
+  GemmArgs g = gemm_args(d.dtype, xn, ldx, xs, w->layers[l].wgu, M, 2 * d.d_ff, d.d_model, act, ld_act);
+  g.ostride = act_os;
   AF_TRY(with_splits(w, g));
   return timed(w, AF_K_GEMM_GATEUP, s, [&] { return launch_gemm(d.dtype, EPI_SWIGLU, g, s); });
 }
 
-af_status step_down(af_weights* w, int l, const void* act, int ld_act, void* hidden, int M, hipStream_t s) {
+af_status step_down(af_weights* w, int l, const void* act, int ld_act, long as, void* hidden, int M, hipStream_t s) {
   const af_model_desc& d = w->d;
-  GemmArgs g = gemm_args(d.dtype, act, ld_act, w->layers[l].wdown, M, d.d_model, d.d_ff, hidden, d.d_model);
+  GemmArgs g = gemm_args(d.dtype, act, ld_act, as, w->layers[l].wdown, M, d.d_model, d.d_ff, hidden, d.d_model);
   g.resid = hidden;
   g.ldr = d.d_model;
   AF_TRY(with_splits(w, g));
@@ -503,24 +512,25 @@ af_status step_down(af_weights* w, int l, const void* act, int ld_act, void* hid
 }
 
 af_status step_norm(af_weights* w, const void* x, int ldx, const int32_t* rows, const void* g, void* y, int ldy,
-                    int n_rows, hipStream_t s) {
+                    long ys, int n_rows, hipStream_t s) {
   const af_model_desc& d = w->d;
   return timed(w, AF_K_RMSNORM, s, [&] {
-    return launch_rmsnorm(d.dtype, x, ldx, rows, g, y, ldy, n_rows, d.d_model, d.rms_eps, s);
+    return launch_rmsnorm(d.dtype, x, ldx, rows, g, y, ldy, ys, n_rows, d.d_model, d.rms_eps, s);
   });
 }
 
 af_status layer_forward(af_weights* w, int l, void* hidden, int M, af_ring* ring, const DevTables& t, hipStream_t s) {
   const Layer& L = w->layers[l];
   const int D = w->d.d_model, ldD = w->ldD, ldF = w->ldF;
-  AF_TRY(step_norm(w, hidden, D, nullptr, L.attn_norm, w->xn, ldD, M, s));
-  AF_TRY(step_qkv(w, l, w->xn, ldD, M, ring, t, w->q, ldD, s));
-  AF_TRY(step_attention(w, w->d.dtype, ring, l, w->q, ldD, w->attn, ldD, t, s));
+  const long xD = w->xs_D, xF = w->xs_F;  // 0 (row-major) for fp32
+  AF_TRY(step_norm(w, hidden, D, nullptr, L.attn_norm, w->xn, ldD, xD, M, s));
+  AF_TRY(step_qkv(w, l, w->xn, ldD, xD, M, ring, t, w->q, ldD, s));
+  AF_TRY(step_attention(w, w->d.dtype, ring, l, w->q, ldD, w->attn, ldD, xD, t, s));
   // InPlaceKVShift: no device work; the slot rotation lives in the ring bookkeeping.
-  AF_TRY(step_o(w, l, w->attn, ldD, hidden, M, s));
-  AF_TRY(step_norm(w, hidden, D, nullptr, L.mlp_norm, w->xn, ldD, M, s));
-  AF_TRY(step_gate_up(w, l, w->xn, ldD, w->act, ldF, M, s));
-  AF_TRY(step_down(w, l, w->act, ldF, hidden, M, s));
+  AF_TRY(step_o(w, l, w->attn, ldD, xD, hidden, M, s));
+  AF_TRY(step_norm(w, hidden, D, nullptr, L.mlp_norm, w->xn, ldD, xD, M, s));
+  AF_TRY(step_gate_up(w, l, w->xn, ldD, xD, w->act, ldF, xF, M, s));
+  AF_TRY(step_down(w, l, w->act, ldF, xF, hidden, M, s));
   return AF_OK;
 }
 
@@ -528,9 +538,10 @@ af_status lm_head(af_weights* w, const void* hidden, const DevTables& t, float* 
                   hipStream_t s) {
   const af_model_desc& d = w->d;
   if (t.n_emit == 0 || (!out_logits && !out_tokens)) return AF_OK;
-  AF_TRY(step_norm(w, hidden, d.d_model, t.emit_rows, w->final_norm, w->emit_norm, w->ldD, t.n_emit, s));
+  AF_TRY(step_norm(w, hidden, d.d_model, t.emit_rows, w->final_norm, w->emit_norm, w->ldD, w->xs_D, t.n_emit, s));
   float* logits = out_logits ? out_logits : w->logits_ws;
-  GemmArgs g = gemm_args(d.dtype, w->emit_norm, w->ldD, w->lm_head, t.n_emit, d.vocab, d.d_model, logits, d.vocab);
+  GemmArgs g = gemm_args(d.dtype, w->emit_norm, w->ldD, w->xs_D, w->lm_head, t.n_emit, d.vocab, d.d_model, logits,
+                         d.vocab);
   AF_TRY(with_splits(w, g));
   AF_TRY(timed(w, AF_K_LM_HEAD, s, [&] { return launch_gemm(d.dtype, EPI_STORE_F32, g, s); }));
   if (out_tokens)
@@ -600,6 +611,10 @@ extern "C" af_status af_weights_create(const af_model_desc* desc, const void* co
   w->es = dtype_size(d.dtype);
   w->ldD = d.d_model + STRIDE_PAD_BYTES / (int)w->es;
   w->ldF = d.d_ff + STRIDE_PAD_BYTES / (int)w->es;
+  if (d.dtype == AF_BF16) {
+    w->xs_D = frag_astride(padk(d.d_model));
+    w->xs_F = frag_astride(padk(d.d_ff));
+  }
   hipStream_t s = (hipStream_t)hip_stream;
   const size_t es = w->es;
   const int D = d.d_model, F = d.d_ff, V = d.vocab, hd = d.head_dim;
@@ -661,7 +676,8 @@ extern "C" af_status af_weights_create(const af_model_desc* desc, const void* co
   const int Dp = padk(D), Fp = padk(F);
   auto pack = [&](void** dst, const void* const* src_d, const int32_t* map, int N, int K, int Kp) -> af_status {
     const long bs = frag_bstride(Kp, d.dtype);
-    AF_TRY(dev_alloc(w, dst, (size_t)(N / 16) * bs * es));
+    const int nc = frag_ncols(d.dtype);
+    AF_TRY(dev_alloc(w, dst, (size_t)((N + nc - 1) / nc) * bs * es));
     AF_HIP(launch_frag_pack(d.dtype, *dst, bs, src_d, map, N, K, Kp, s));
     return AF_OK;
   };
@@ -768,7 +784,7 @@ extern "C" af_status af_op_rmsnorm(int32_t dtype, const void* x, const void* g, 
     set_error("af_op_rmsnorm: bad argument");
     return AF_ERR_INVALID_ARG;
   }
-  AF_HIP(launch_rmsnorm(dtype, x, D, nullptr, g, y, D, M, D, eps, (hipStream_t)hip_stream));
+  AF_HIP(launch_rmsnorm(dtype, x, D, nullptr, g, y, D, 0, M, D, eps, (hipStream_t)hip_stream));
   return AF_OK;
 }
 
@@ -786,20 +802,33 @@ extern "C" af_status af_op_linear(int32_t dtype, const void* x, const void* wt, 
   }
   // the caller's weight is row-major [N, K]: fragment-tile a private copy (synchronous)
   hipStream_t s = (hipStream_t)hip_stream;
-  const int Kp = padk(K);
-  void* wf = nullptr;
+  const int Kp = padk(K), nc = frag_ncols(dtype);
+  void *wf = nullptr, *xf = nullptr;
   const void** src_d = nullptr;
   const long bs = frag_bstride(Kp, dtype);
-  AF_HIP(hipMalloc(&wf, (size_t)(N / 16) * bs * dtype_size(dtype)));
+  const long xs = dtype == AF_BF16 ? frag_astride(Kp) : 0;  // bf16 reads fragment-tiled activations
+  AF_HIP(hipMalloc(&wf, (size_t)((N + nc - 1) / nc) * bs * dtype_size(dtype)));
   hipError_t e = hipMalloc((void**)&src_d, sizeof(void*));
   if (e == hipSuccess) e = hipMemcpy(src_d, &wt, sizeof(void*), hipMemcpyHostToDevice);
   if (e == hipSuccess) e = launch_frag_pack(dtype, wf, bs, src_d, nullptr, N, K, Kp, s);
+  if (e == hipSuccess && xs) {
+    e = hipMalloc(&xf, (size_t)((M + 31) / 32) * xs * 2);
+    if (e == hipSuccess) e = launch_to_frag(dtype, x, K, M, K, Kp, xf, xs, s);
+  }
+  float* part = nullptr;
   if (e == hipSuccess) {
-    GemmArgs g = gemm_args(dtype, x, K, wf, M, N, K, y, N);
-    e = launch_gemm(dtype, EPI_STORE, g, s);
+    GemmArgs g = gemm_args(dtype, xs ? xf : x, K, xs, wf, M, N, K, y, N);
+    g.splits = gemm_splits(dtype, M, N, Kp);  // the split the model path would use for this shape
+    if (g.splits > 1) {
+      e = hipMalloc((void**)&part, (size_t)g.splits * M * N * 4);
+      g.partial = part;
+    }
+    if (e == hipSuccess) e = launch_gemm(dtype, EPI_STORE, g, s);
   }
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   (void)hipFree(wf);
+  if (xf) (void)hipFree(xf);
+  if (part) (void)hipFree(part);
   if (src_d) (void)hipFree(src_d);
   if (e != hipSuccess) {
     set_error("af_op_linear: %s", hipGetErrorString(e));
@@ -807,6 +836,17 @@ extern "C" af_status af_op_linear(int32_t dtype, const void* x, const void* wt, 
   }
   return AF_OK;
 }
+
+namespace {
+// The single-step entry points take row-major activations.  For bf16 the projection GEMMs read
+// fragment-tiled ones: copy the input into the workspace buffer `dst` (stride xs) first.
+af_status stage_input(af_weights* w, const void*& x, int K, int M, void* dst, long xs, hipStream_t s) {
+  if (!xs) return AF_OK;
+  AF_HIP(launch_to_frag(w->d.dtype, x, K, M, K, padk(K), dst, xs, s));
+  x = dst;
+  return AF_OK;
+}
+}  // namespace
 
 extern "C" af_status af_op_qkv_rope_write(af_weights* w, int32_t layer, const void* xn, int32_t M,
                                           const af_segment* segs, int32_t n_seg, af_ring* ring, void* q_out,
@@ -819,7 +859,8 @@ extern "C" af_status af_op_qkv_rope_write(af_weights* w, int32_t layer, const vo
   hipStream_t s = (hipStream_t)hip_stream;
   StepDesc sd;
   AF_TRY(prepare_step(w, ring, segs, n_seg, M, layer + 1, sd, s));
-  return step_qkv(w, layer, xn, w->d.d_model, M, ring, dev_tables(w, sd), q_out, w->d.d_model, s);
+  AF_TRY(stage_input(w, xn, w->d.d_model, M, w->xn, w->xs_D, s));
+  return step_qkv(w, layer, xn, w->d.d_model, w->xs_D, M, ring, dev_tables(w, sd), q_out, w->d.d_model, s);
 }
 
 extern "C" af_status af_op_attention(af_ring* ring, int32_t layer, const void* q, int32_t M, const af_segment* segs,
@@ -847,7 +888,7 @@ extern "C" af_status af_op_attention(af_ring* ring, int32_t layer, const void* q
     t.n_tiles = sd.n_tiles;
     t.n_emit = sd.n_emit;
     const int ld = ring->d.n_kv_heads * ring->d.head_dim;
-    st = step_attention(nullptr, ring->d.dtype, ring, layer, q, ld, o, ld, t, s);
+    st = step_attention(nullptr, ring->d.dtype, ring, layer, q, ld, o, ld, 0, t, s);
     if (st == AF_OK) e = hipStreamSynchronize(s);
   }
   (void)hipFree(dd);
@@ -865,7 +906,10 @@ extern "C" af_status af_op_o_proj_residual(af_weights* w, int32_t layer, const v
     set_error("af_op_o_proj_residual: bad argument");
     return AF_ERR_INVALID_ARG;
   }
-  return step_o(w, layer, o, w->d.d_model, hidden, M, (hipStream_t)hip_stream);
+  hipStream_t s = (hipStream_t)hip_stream;
+  AF_TRY(ensure_workspace(w, M, 0));
+  AF_TRY(stage_input(w, o, w->d.d_model, M, w->attn, w->xs_D, s));
+  return step_o(w, layer, o, w->d.d_model, w->xs_D, hidden, M, s);
 }
 
 extern "C" af_status af_op_gate_up_swiglu(af_weights* w, int32_t layer, const void* xn, void* act, int32_t M,
@@ -875,7 +919,10 @@ extern "C" af_status af_op_gate_up_swiglu(af_weights* w, int32_t layer, const vo
     set_error("af_op_gate_up_swiglu: bad argument");
     return AF_ERR_INVALID_ARG;
   }
-  return step_gate_up(w, layer, xn, w->d.d_model, act, w->d.d_ff, M, (hipStream_t)hip_stream);
+  hipStream_t s = (hipStream_t)hip_stream;
+  AF_TRY(ensure_workspace(w, M, 0));
+  AF_TRY(stage_input(w, xn, w->d.d_model, M, w->xn, w->xs_D, s));
+  return step_gate_up(w, layer, xn, w->d.d_model, w->xs_D, act, w->d.d_ff, 0, M, s);
 }
 
 extern "C" af_status af_op_down_residual(af_weights* w, int32_t layer, const void* act, void* hidden, int32_t M,
@@ -885,7 +932,10 @@ extern "C" af_status af_op_down_residual(af_weights* w, int32_t layer, const voi
     set_error("af_op_down_residual: bad argument");
     return AF_ERR_INVALID_ARG;
   }
-  return step_down(w, layer, act, w->d.d_ff, hidden, M, (hipStream_t)hip_stream);
+  hipStream_t s = (hipStream_t)hip_stream;
+  AF_TRY(ensure_workspace(w, M, 0));
+  AF_TRY(stage_input(w, act, w->d.d_ff, M, w->act, w->xs_F, s));
+  return step_down(w, layer, act, w->d.d_ff, w->xs_F, hidden, M, s);
 }
 
 extern "C" af_status af_op_lm_head_argmax(af_weights* w, const void* hidden, int32_t M, const af_segment* segs,
