@@ -143,6 +143,86 @@ __device__ __forceinline__ void epi_pair(const GemmArgs& a, int m, int c, float 
   }
 }
 
+// Grouped epilogues (the bf16 GEMM, and the split-K reduction of both kernels): one call
+// handles 8 consecutive output columns of a row with 16-byte (bf16) or 32-byte (fp32) accesses.
+template <typename T>
+__device__ __forceinline__ void load8(const T* p, T* r) {
+  if constexpr (sizeof(T) == 2) {
+    *(uint4*)r = *(const uint4*)p;
+  } else {
+    *(uint4*)r = *(const uint4*)p;
+    *(uint4*)(r + 4) = *(const uint4*)(p + 4);
+  }
+}
+template <typename T>
+__device__ __forceinline__ void store8(T* p, const T* r) {
+  if constexpr (sizeof(T) == 2) {
+    *(uint4*)p = *(const uint4*)r;
+  } else {
+    *(uint4*)p = *(const uint4*)r;
+    *(uint4*)(p + 4) = *(const uint4*)(r + 4);
+  }
+}
+
+// Columns nc .. nc+7 (nc % 8 == 0) of row m.
+template <typename T, int EPI>
+__device__ __forceinline__ void epi_group8(const GemmArgs& a, int m, int nc, const float* v) {
+  if constexpr (EPI == EPI_STORE_F32) {
+    store8<float>((float*)a.out + (size_t)m * a.ldo + nc, v);
+  } else {
+    T r[8];
+    if constexpr (EPI == EPI_RESID) {  // out may alias resid: each element is read, then written, by one thread
+      T res[8];
+      load8<T>((const T*)a.resid + (size_t)m * a.ldr + nc, res);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) r[e] = from_f<T>(to_f(res[e]) + v[e]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) r[e] = from_f<T>(v[e]);
+    }
+    store8<T>((T*)a.out + (size_t)m * a.ldo + nc, r);
+  }
+}
+
+// The 16-column group starting at c (c % 16 == 0): a-columns c .. c+7, partners c+8 .. c+15.
+template <typename T, int EPI>
+__device__ __forceinline__ void epi_group16(const GemmArgs& a, int m, int c, const float* va, const float* vb) {
+  T r0[8], r1[8];
+  if constexpr (EPI == EPI_SWIGLU) {
+    const int f = (c >> 4) * 8;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) r0[e] = from_f<T>(va[e] / (1.0f + __expf(-va[e])) * vb[e]);
+    store8<T>((T*)a.out + (a.ostride > 0 ? frag_off(m, f, a.ostride) : (size_t)m * a.ldo + f), r0);
+  } else {  // EPI_QKV: rotary pairs (dj + e, dj + e + hd/2), e < 8
+    const int D = a.d_model, hd = a.head_dim, half = hd >> 1;
+    const int region = c / D, cr = c - region * D;
+    const int h = cr / hd, dj = ((cr - h * hd) >> 4) * 8;
+    const int slot = a.row_sp[2 * m], pos = a.row_sp[2 * m + 1];
+    T* dst;
+    if (region == 2) {
+      dst = (T*)a.ring_v + (((size_t)slot * a.n_heads + h) * a.max_pos + pos) * hd;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        r0[e] = from_f<T>(va[e]);
+        r1[e] = from_f<T>(vb[e]);
+      }
+    } else {
+      float cs[16];
+      load8<float>(a.rope_cs + ((size_t)pos * half + dj) * 2, cs);
+      load8<float>(a.rope_cs + ((size_t)pos * half + dj) * 2 + 8, cs + 8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        r0[e] = from_f<T>(va[e] * cs[2 * e] - vb[e] * cs[2 * e + 1]);
+        r1[e] = from_f<T>(vb[e] * cs[2 * e] + va[e] * cs[2 * e + 1]);
+      }
+      dst = region == 0 ? (T*)a.out + (size_t)m * a.ldo + h * hd
+                        : (T*)a.ring_k + (((size_t)slot * a.n_heads + h) * a.max_pos + pos) * hd;
+    }
+    store8<T>(dst + dj, r0);
+    store8<T>(dst + dj + half, r1);
+  }
+}
+
 // Tile configuration: BM rows (all packed rows for M <= 288) x four waves of WTN columns;
 // PF weight k steps in flight per wave; DA activation stages in flight; OCC workgroups per CU.
 template <int BM_, int WTN_, int PF_, int DA_, int OCC_>
@@ -266,29 +346,32 @@ __global__ __launch_bounds__(256, C::OCC) void gemm_kernel(GemmArgs a) {
   });
 }
 
-// Sums the split-K partials in split order and applies the epilogue; one thread per output
-// element (or per rotary/SwiGLU pair).
+// Sums the split-K partials in split order and applies the epilogue; one thread per 8 output
+// columns of a row (per 16-column pair group for the paired epilogues).
 template <typename T, int EPI>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
   constexpr bool paired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
-  const int per_row = paired ? a.N / 2 : a.N;
+  constexpr int W = paired ? 16 : 8;  // columns per thread
+  const int per_row = a.N / W;
   const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (size_t)a.M * per_row) return;
-  const int m = (int)(idx / per_row), p = (int)(idx % per_row);
+  const int m = (int)(idx / per_row), c = (int)(idx % per_row) * W;
   const size_t plane = (size_t)a.M * a.N;
-  if constexpr (paired) {
-    const int c = (p >> 3) * 16 + (p & 7);
-    float va = 0.f, vb = 0.f;
-    for (int s = 0; s < a.splits; ++s) {
-      va += a.partial[s * plane + (size_t)m * a.N + c];
-      vb += a.partial[s * plane + (size_t)m * a.N + c + 8];
-    }
-    epi_pair<T, EPI>(a, m, c, va, vb);
-  } else {
-    float v = 0.f;
-    for (int s = 0; s < a.splits; ++s) v += a.partial[s * plane + (size_t)m * a.N + p];
-    epi_single<T, EPI>(a, m, p, v);
+  float v[W];
+#pragma unroll
+  for (int e = 0; e < W; ++e) v[e] = 0.f;
+  for (int sp = 0; sp < a.splits; ++sp) {
+    float t[W];
+    const float* src = a.partial + sp * plane + (size_t)m * a.N + c;
+    load8<float>(src, t);
+    if constexpr (paired) load8<float>(src + 8, t + 8);
+#pragma unroll
+    for (int e = 0; e < W; ++e) v[e] += t[e];
   }
+  if constexpr (paired)
+    epi_group16<T, EPI>(a, m, c, v, v + 8);
+  else
+    epi_group8<T, EPI>(a, m, c, v);
 }
 
 template <typename T, typename C>
@@ -309,7 +392,8 @@ static hipError_t gemm_launch_cfg(int epi, const GemmArgs& a, hipStream_t s) {
 template <typename T>
 static hipError_t reduce_launch(int epi, const GemmArgs& a, hipStream_t s) {
   const bool paired = epi == EPI_SWIGLU || epi == EPI_QKV;
-  const size_t n = (size_t)a.M * (paired ? a.N / 2 : a.N);
+  if (a.N % 16) return hipErrorInvalidValue;
+  const size_t n = (size_t)a.M * (a.N / (paired ? 16 : 8));
   dim3 grid((unsigned)((n + 255) / 256)), block(256);
   switch (epi) {
     case EPI_STORE: hipLaunchKernelGGL((splitk_reduce_kernel<T, EPI_STORE>), grid, block, 0, s, a); break;
@@ -451,25 +535,42 @@ __global__ __launch_bounds__(256, 1) void gemm32_kernel(GemmArgs a) {
 #pragma unroll
   for (int p = 0; p < PFB; ++p) asm volatile("" : "+v"(rb[p]));
 
-  // ---------------- epilogue: acc[i][r] is row 32 (mt FM + i) + 8 (r / 4) + 4 (lane / 32) + r % 4
-  // of column 32 nb + lane % 32
-  const int nc = nb_raw * 32 + (lane & 31);
-  const bool col_ok = nb_raw < n_blocks && nc < a.N;
+  // ---------------- epilogue.  The fp32 tile goes through LDS (the stage buffers hold exactly
+  // 32 FM x 128 floats), then every thread handles 8 consecutive columns of a row (a 16-column
+  // pair group for the paired epilogues) with vector accesses.  acc[i][r] is tile row
+  // 32 i + 8 (r / 4) + 4 (lane / 32) + r % 4, tile column 32 nw + lane % 32.
+  static_assert(32 * FM * 128 * 4 == (int)sizeof(As), "epilogue tile must fill the stage buffers");
+  float* T_ = (float*)&As[0][0];
+  __syncthreads();  // every wave's last DMA has landed (vmcnt(0) above) and its LDS reads are done
   static_for<0, FM>([&](auto i) {
     static_for<0, 16>([&](auto r) {
       constexpr int R = decltype(r)::value;
-      const int m = (mt * FM + (int)decltype(i)::value) * 32 + 8 * (R / 4) + 4 * (lane >> 5) + (R % 4);
-      const float v = acc[i][R];
-      const bool ok = col_ok && m < a.M;
-      if constexpr (EPI == EPI_SWIGLU || EPI == EPI_QKV) {
-        const float partner = __shfl_xor(v, 8);  // all lanes take part
-        if (S == 1 && ok && (lane & 8) == 0) epi_pair<bf16, EPI>(a, m, nc, v, partner);
-      } else {
-        if (S == 1 && ok) epi_single<bf16, EPI>(a, m, nc, v);
-      }
-      if (S > 1 && ok) a.partial[((size_t)sp * a.M + m) * a.N + nc] = v;
+      const int row = (int)decltype(i)::value * 32 + 8 * (R / 4) + 4 * (lane >> 5) + (R % 4);
+      T_[row * 128 + nw * 32 + (lane & 31)] = acc[i][R];
     });
   });
+  __syncthreads();
+  constexpr bool paired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
+  constexpr int W = paired ? 16 : 8;        // columns per item
+  constexpr int ITEMS = 32 * FM * (128 / W);
+  const int m0 = mt * FM * 32, n0 = nt * 128;
+  for (int it = tid; it < ITEMS; it += 256) {
+    const int row = it / (128 / W), col = (it % (128 / W)) * W;
+    const int m = m0 + row, nc = n0 + col;
+    if (m >= a.M || nc >= a.N) continue;  // N % 16 == 0: a group is wholly inside or outside
+    float v[W];
+#pragma unroll
+    for (int e = 0; e < W; e += 4) *(f32x4*)&v[e] = *(const f32x4*)&T_[row * 128 + col + e];
+    if (S > 1) {
+      float* dst = a.partial + ((size_t)sp * a.M + m) * a.N + nc;
+#pragma unroll
+      for (int e = 0; e < W; e += 4) *(f32x4*)(dst + e) = *(const f32x4*)&v[e];
+    } else if constexpr (paired) {
+      epi_group16<bf16, EPI>(a, m, nc, v, v + 8);
+    } else {
+      epi_group8<bf16, EPI>(a, m, nc, v);
+    }
+  }
 }
 
 static int fm_for(int M) {
