@@ -44,6 +44,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
     p.add_argument("--no-timing-pass", action="store_true")
+    p.add_argument("--no-extra", action="store_true",
+                   help="skip the sequential-baseline and decode-heavy attention measurements")
     p.add_argument("--copy-calibration", action="store_true",
                    help="before warm-up, run one streaming copy of COPY_BYTES (read once, written once) "
                         "whose hardware-counter readings scale the FETCH_SIZE / WRITE_SIZE of the others")
@@ -163,6 +165,84 @@ def attention_bytes(segs, H, hd):
     kv = sum((s[3] + s[1]) * H * hd * 2 * b for s in segs)
     M = sum(s[1] for s in segs)
     return kv + 2 * M * H * hd * b
+
+
+# ----------------------------------------------------------------------------- extra measurements
+def sequential_baseline(af, w, shape, pids, pool, K, n_req=6, warm=2):
+    """The plain per-request schedule on the same kernels (the paper's baseline): each request
+    alone, a 276-row prefill then K - 1 single-row decode forwards through all layers, with the
+    greedy token fed back on the device.  Returns ms per request (one action chunk)."""
+    import torch
+    L_P = int(pids.numel())
+    ring = af.Ring(shape.n_layers, 2, L_P + K, shape.n_heads, shape.head_dim, dtype=torch.bfloat16)
+    hidden = torch.empty((L_P, shape.d_model), dtype=torch.bfloat16, device="cuda")
+    toks = torch.zeros(K, dtype=torch.int32, device="cuda")
+    times = []
+    for r in range(warm + n_req):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        s = ring.append(r, L_P)
+        s.flags = af.AF_SEG_EMIT
+        af.packed_forward(w, pids, pool[r % len(pool)][:L_P], [s], ring, hidden, None, toks[0:1])
+        for k in range(1, K):
+            s = ring.append(r, 1)
+            s.flags = af.AF_SEG_EMIT
+            af.packed_forward(w, toks[k - 1:k], None, [s], ring, hidden[:1], None, toks[k:k + 1])
+        ring.release(r)
+        torch.cuda.synchronize()
+        if r >= warm:
+            times.append(time.perf_counter() - t0)
+    ring.close()
+    return sorted(times)[len(times) // 2] * 1e3
+
+
+def decode_heavy_attention(af, w, shape, n_pipe=8, K=8, L_P=276, reps=10):
+    """Attention of the multi-pipeline stress step (n_pipe pipelines x (L_P prefill + K - 1
+    decode rows), pipeline-major, one slot per request: 64 slots x 288), timed by the library's
+    per-kernel HIP events inside one layer forward (layer 0 of the loaded model); also the
+    decode rows alone.  Ring history is seeded N(0, 1)."""
+    import torch
+    import workload as wl
+    H, hd, D = shape.n_heads, shape.head_dim, shape.d_model
+    n_slots, max_pos = n_pipe * K, 288
+    ring = af.Ring(1, n_slots, max_pos, H, hd, dtype=torch.bfloat16)
+    segs_all, segs_dec, row, row_d = [], [], 0, 0
+    for p in range(n_pipe):
+        rid0 = 10_000 + p * K
+        s = ring.append(rid0, L_P)
+        segs_all.append((row, L_P, s.slot, 0, rid0, af.AF_SEG_EMIT))
+        row += L_P
+        for st in range(1, K):
+            rid = rid0 + st
+            ring.append(rid, L_P + st - 1)
+            s = ring.append(rid, 1)
+            segs_all.append((row, 1, s.slot, s.pos0, rid, af.AF_SEG_EMIT))
+            segs_dec.append((row_d, 1, s.slot, s.pos0, rid, af.AF_SEG_EMIT))
+            row += 1
+            row_d += 1
+    for sl in range(n_slots):
+        kv = wl.draw(("ring history", sl), (2, max_pos, H, hd), device="cuda", dtype=torch.bfloat16)
+        ring.write_kv(0, sl, 0, kv[0], kv[1])
+    out = {}
+    for name, segs, M in (("stress_step", segs_all, row), ("decode_rows_only", segs_dec, row_d)):
+        hid = wl.draw(("stress hidden", name), (M, D), device="cuda", dtype=torch.bfloat16)
+        af.packed_layer_forward(w, 0, hid.clone(), segs, ring)
+        torch.cuda.synchronize()
+        w.timing_enable((1 << af.AF_K_COUNT) - 1)
+        for _ in range(reps):
+            af.packed_layer_forward(w, 0, hid.clone(), segs, ring)
+        torch.cuda.synchronize()
+        tm = w.timing_read()
+        w.timing_enable(0)
+        at_ms = tm["attention"][0] / tm["attention"][1]
+        nbytes = attention_bytes(segs, H, hd)
+        layer_ms = sum(ms for ms, n in tm.values()) / reps
+        out[name] = {"M": M, "attention_us": round(at_ms * 1e3, 2), "bytes": nbytes,
+                     "GB/s": round(nbytes / (at_ms * 1e-3) / 1e9, 1),
+                     "frac_hbm": round(nbytes / (at_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+                     "layer_kernels_ms": round(layer_ms, 4)}
+    ring.close()
+    return out
 
 
 # ----------------------------------------------------------------------------- cpu baseline
@@ -333,6 +413,16 @@ def main():
         out["timing_pass_ms_per_step"] = round(t_inst / args.steps * 1e3, 4)
         log(f"timing pass: {json.dumps(per_step)}")
 
+    if not args.no_extra:
+        log("sequential baseline (one request at a time, same kernels)")
+        seq_ms = sequential_baseline(af, w, shape, pids, pool, K)
+        out["sequential_baseline"] = {
+            "ms_per_request": round(seq_ms, 3), "requests_per_s": round(1e3 / seq_ms, 3),
+            "packed_speedup": round(steps_s / (1e3 / seq_ms), 3),
+            "note": "one request = 276-row prefill + 6 single-row decodes through 32 layers; the packed "
+                    "pipeline completes one request per step"}
+        log("decode-heavy attention (8 pipelines x (276 + 7), 64 slots)")
+        out["attention_stress"] = decode_heavy_attention(af, w, shape)
     ring.close()
     w.close()
     torch.cuda.empty_cache()

@@ -72,7 +72,8 @@ struct AttnArgs {
   const void* ring_k;  // this layer's key region
   const void* ring_v;
   const DevSeg* segs;
-  const int32_t* tiles;  // [n_tiles][2]: (segment, first row in segment)
+  const int32_t* tiles;  // [n_tiles][2]: (segment, first row in segment); multi-row tiles first
+  int n_multi;           // tiles of segments with more than one row (the rest are single rows)
   int n_heads, max_pos, ldq, ldo;  // row strides of q and o (>= H*hd)
   long ostride;              // > 0: o is written fragment-tiled (32-row blocks ostride apart)
   float scale_log2;          // log2(e) / sqrt(hd)

@@ -635,6 +635,130 @@ hipError_t launch_gemm(int dtype, int epi, const GemmArgs& a, hipStream_t s) {
 // each lane holds scores of one query and the probabilities feed the P.V MFMA as its B
 // operand without a lane exchange; softmax is online in the exp2 domain with the running
 // max reduced across the four lanes that share a query.
+// Single-row segments (decode steps), one workgroup per (segment, head): one query against
+// its slot's keys 0 .. pos0.  The four waves take chunks of 64 keys in turn.  A chunk issues all
+// of its loads first (one memory latency per chunk): lane l's key c*64 + l for the score, and
+// for the value sum VEC dims of one dim group (l % DG) over the keys of its key group
+// (l / DG + KG t), so every access is a 16-byte load.  Scores are fp32 dot products of the
+// stored vectors (bf16 pairs through v_dot2); the softmax is online in the exp2 domain; the
+// waves' (max, sum, output) are merged through LDS.  Separate from the tiled kernel so each
+// keeps its own register budget.
+template <typename T>
+__device__ __forceinline__ float dot_vec(const uint4& k, const uint4& q, float acc) {
+  if constexpr (sizeof(T) == 2) {
+    typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
+    const unsigned kk[4] = {k.x, k.y, k.z, k.w}, qq[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, kk[i]), __builtin_bit_cast(bf16x2, qq[i]), acc,
+                                            false);
+    return acc;
+  } else {
+    const float* kf = (const float*)&k;
+    const float* qf = (const float*)&q;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc += kf[i] * qf[i];
+    return acc;
+  }
+}
+
+template <typename T, int HD>
+__global__ __launch_bounds__(256) void attention_decode_kernel(AttnArgs a) {
+  constexpr int VEC = Chunk<T>::N;  // elements per 16 bytes
+  constexpr int DG = HD / VEC;      // dim groups
+  constexpr int KG = 64 / DG;       // key groups per 64-key chunk
+  static_assert(DG <= 64 && 64 % DG == 0, "head_dim");
+  __shared__ float wm[4], wl[4];
+  __shared__ __attribute__((aligned(16))) float wo[4][HD];
+  const int seg_i = a.tiles[2 * (a.n_multi + blockIdx.x)];
+  const int h = blockIdx.y;
+  const DevSeg sg = a.segs[seg_i];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int kv_len = sg.pos0 + 1;
+  const size_t slot_off = ((size_t)sg.slot * a.n_heads + h) * a.max_pos * HD;
+  const T* __restrict__ Kg = (const T*)a.ring_k + slot_off;
+  const T* __restrict__ Vg = (const T*)a.ring_v + slot_off;
+  const uint4* qrow = (const uint4*)((const T*)a.q + (size_t)sg.q_start * a.ldq + h * HD);
+  uint4 qv[DG];  // the query, the same in every lane
+#pragma unroll
+  for (int pc = 0; pc < DG; ++pc) qv[pc] = qrow[pc];
+
+  const int dg = lane % DG, kgrp = lane / DG;
+  float m_run = -INFINITY, l_run = 0.f, o[VEC];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) o[e] = 0.f;
+  for (int c = wave; c * 64 < kv_len; c += 4) {
+    // lane l scores key c*64 + l; past kv_len it reads a clamped valid key and scores -inf
+    const int j = c * 64 + lane;
+    const uint4* krow = (const uint4*)(Kg + (size_t)min(j, kv_len - 1) * HD);
+    uint4 kv[DG], vv[64 / KG];
+#pragma unroll
+    for (int pc = 0; pc < DG; ++pc) kv[pc] = krow[pc];
+#pragma unroll
+    for (int t = 0; t < 64 / KG; ++t)
+      vv[t] = *(const uint4*)(Vg + (size_t)min(c * 64 + kgrp + KG * t, kv_len - 1) * HD + dg * VEC);
+    float dot = 0.f;
+#pragma unroll
+    for (int pc = 0; pc < DG; ++pc) dot = dot_vec<T>(kv[pc], qv[pc], dot);
+    const float sc = j < kv_len ? dot * a.scale_log2 : -INFINITY;
+    float cm = sc;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) cm = fmaxf(cm, __shfl_xor(cm, off));
+    const float m_new = fmaxf(m_run, cm);
+    const float p = exp2f(sc - m_new);
+    float ps = p;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) ps += __shfl_xor(ps, off);
+    const float corr = exp2f(m_run - m_new);  // 0 on the first chunk (m_run = -inf)
+    l_run = l_run * corr + ps;
+    m_run = m_new;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) o[e] *= corr;
+    // lane covers dims [VEC dg, +VEC) of keys c*64 + kgrp + KG t (masked keys carry p = 0)
+#pragma unroll
+    for (int t = 0; t < 64 / KG; ++t) {
+      const float pj = __shfl(p, kgrp + KG * t);
+      T vt[VEC];
+      __builtin_memcpy(vt, &vv[t], 16);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) o[e] += pj * to_f(vt[e]);
+    }
+  }
+  // ---- merge the key groups of the wave, then the four waves
+#pragma unroll
+  for (int off = DG; off < 64; off <<= 1)
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) o[e] += __shfl_xor(o[e], off);
+  if (lane == 0) {
+    wm[wave] = m_run;
+    wl[wave] = l_run;
+  }
+  if (lane < DG)
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) wo[wave][dg * VEC + e] = o[e];
+  __syncthreads();
+  if (wave == 0 && lane < DG) {
+    const float M = fmaxf(fmaxf(wm[0], wm[1]), fmaxf(wm[2], wm[3]));
+    float L = 0.f, acc[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float f = wm[w] == -INFINITY ? 0.f : exp2f(wm[w] - M);  // a wave with no chunk holds nothing
+      L += wl[w] * f;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) acc[e] += wo[w][dg * VEC + e] * f;
+    }
+    const float inv = 1.0f / L;
+    T r[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) r[e] = from_f<T>(acc[e] * inv);
+    const int k0 = h * HD + dg * VEC;
+    T* dst = a.ostride > 0 ? (T*)a.o + frag_off(sg.q_start, k0, a.ostride) : (T*)a.o + (size_t)sg.q_start * a.ldo + k0;
+    *(uint4*)dst = *(const uint4*)r;
+  }
+}
+
 template <typename T, int HD>
 __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a) {
   constexpr int VEC = Chunk<T>::N;
@@ -786,17 +910,25 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a) {
   }
 }
 
+template <typename T, int HD>
+static void attention_launch(const AttnArgs& a, int n_tiles, hipStream_t s) {
+  if (a.n_multi > 0)
+    hipLaunchKernelGGL((attention_kernel<T, HD>), dim3(a.n_multi, a.n_heads), dim3(256), 0, s, a);
+  if (n_tiles > a.n_multi)
+    hipLaunchKernelGGL((attention_decode_kernel<T, HD>), dim3(n_tiles - a.n_multi, a.n_heads), dim3(256), 0, s, a);
+}
+
+// tiles[0, n_multi) are query tiles of multi-row segments, tiles[n_multi, n_tiles) the
+// single-row segments.
 hipError_t launch_attention(int dtype, int head_dim, const AttnArgs& a, int n_tiles, hipStream_t s) {
   if (n_tiles <= 0) return hipSuccess;
-  dim3 grid(n_tiles, a.n_heads), block(256);
+  if (a.n_multi < 0 || a.n_multi > n_tiles || (head_dim != 64 && head_dim != 128)) return hipErrorInvalidValue;
   if (dtype == AF_BF16) {
-    if (head_dim == 128) hipLaunchKernelGGL((attention_kernel<bf16, 128>), grid, block, 0, s, a);
-    else if (head_dim == 64) hipLaunchKernelGGL((attention_kernel<bf16, 64>), grid, block, 0, s, a);
-    else return hipErrorInvalidValue;
+    if (head_dim == 128) attention_launch<bf16, 128>(a, n_tiles, s);
+    else attention_launch<bf16, 64>(a, n_tiles, s);
   } else {
-    if (head_dim == 128) hipLaunchKernelGGL((attention_kernel<float, 128>), grid, block, 0, s, a);
-    else if (head_dim == 64) hipLaunchKernelGGL((attention_kernel<float, 64>), grid, block, 0, s, a);
-    else return hipErrorInvalidValue;
+    if (head_dim == 128) attention_launch<float, 128>(a, n_tiles, s);
+    else attention_launch<float, 64>(a, n_tiles, s);
   }
   return hipGetLastError();
 }

@@ -197,7 +197,7 @@ af_status check_segments(const af_ring* ring, const af_segment* segs, int n_seg,
 struct StepDesc {
   std::vector<int32_t> buf;
   size_t off_segs = 0, off_rows = 0, off_tiles = 0, off_emit = 0;
-  int n_tiles = 0, n_emit = 0;
+  int n_tiles = 0, n_multi = 0, n_emit = 0;
 };
 
 void build_desc(const af_segment* segs, int n_seg, int M, StepDesc& sd) {
@@ -205,16 +205,21 @@ void build_desc(const af_segment* segs, int n_seg, int M, StepDesc& sd) {
   int n_emit = 0;
   for (int i = 0; i < n_seg; ++i)
     if (segs[i].flags & AF_SEG_EMIT) emit_idx[i] = n_emit++;
-  // attention work tiles: multi-row segments first, latest (longest-context) tiles first
+  // attention work: query tiles of multi-row segments (largest work first, latest tiles first),
+  // then the single-row segments, which the decode kernel splits over their keys instead
   std::vector<std::pair<int, int>> tiles;
   std::vector<int> by_len(n_seg);
   std::iota(by_len.begin(), by_len.end(), 0);
   std::stable_sort(by_len.begin(), by_len.end(), [&](int a, int b) {
+    const bool ma = segs[a].q_len > 1, mb = segs[b].q_len > 1;
+    if (ma != mb) return ma;
     return (int64_t)segs[a].q_len * (segs[a].pos0 + segs[a].q_len) > (int64_t)segs[b].q_len * (segs[b].pos0 + segs[b].q_len);
   });
+  sd.n_multi = 0;
   for (int i : by_len) {
     const int nt = (segs[i].q_len + ATTN_BQ - 1) / ATTN_BQ;
     for (int t = nt - 1; t >= 0; --t) tiles.push_back({i, t * ATTN_BQ});
+    if (segs[i].q_len > 1) sd.n_multi += nt;
   }
   sd.n_tiles = (int)tiles.size();
   sd.n_emit = n_emit;
@@ -395,7 +400,7 @@ struct DevTables {
   const int32_t* row_sp;
   const int32_t* tiles;
   const int32_t* emit_rows;
-  int n_tiles, n_emit;
+  int n_tiles, n_multi, n_emit;
 };
 
 DevTables dev_tables(const af_weights* w, const StepDesc& sd) {
@@ -405,6 +410,7 @@ DevTables dev_tables(const af_weights* w, const StepDesc& sd) {
   t.tiles = w->desc_dev + sd.off_tiles;
   t.emit_rows = w->desc_dev + sd.off_emit;
   t.n_tiles = sd.n_tiles;
+  t.n_multi = sd.n_multi;
   t.n_emit = sd.n_emit;
   return t;
 }
@@ -475,6 +481,7 @@ af_status step_attention(af_weights* w, int dtype, af_ring* ring, int l, const v
   a.ring_v = (char*)ring->kv + ring->offset(l, 1, 0, 0, 0) * es;
   a.segs = t.segs;
   a.tiles = t.tiles;
+  a.n_multi = t.n_multi;
   a.n_heads = ring->d.n_kv_heads;
   a.max_pos = ring->d.max_pos;
   a.ldq = ldq;
@@ -886,6 +893,7 @@ extern "C" af_status af_op_attention(af_ring* ring, int32_t layer, const void* q
     t.tiles = dd + sd.off_tiles;
     t.emit_rows = dd + sd.off_emit;
     t.n_tiles = sd.n_tiles;
+    t.n_multi = sd.n_multi;
     t.n_emit = sd.n_emit;
     const int ld = ring->d.n_kv_heads * ring->d.head_dim;
     st = step_attention(nullptr, ring->d.dtype, ring, layer, q, ld, o, ld, 0, t, s);
