@@ -442,9 +442,9 @@ static hipError_t gemm_dispatch_f32(int epi, const GemmArgs& a, hipStream_t s) {
 //    4 k steps of FM MFMAs with the next step's LDS reads issued ahead, refilling one weight
 //    slot per step.
 // Splits cover whole units of 4 stages (K is padded to a multiple of 256).
-template <int FM, int EPI>
-__global__ __launch_bounds__(256, 1) void gemm32_kernel(GemmArgs a) {
-  constexpr int NW = 4, KS = 4, NBUF = 4, PFB = 8, BLK = 512;
+template <int FM, int NW, int EPI>
+__global__ __launch_bounds__(64 * NW, 1) void gemm32_kernel(GemmArgs a) {
+  constexpr int KS = 4, NBUF = 4, PFB = 8, BLK = 512;
   constexpr int SB = FM * KS;  // fragment blocks per stage
   constexpr int D = SB / NW;   // DMAs per wave per stage
   constexpr int P = PFB / KS;  // stages of weight lookahead
@@ -539,19 +539,178 @@ __global__ __launch_bounds__(256, 1) void gemm32_kernel(GemmArgs a) {
   // 32 FM x 128 floats), then every thread handles 8 consecutive columns of a row (a 16-column
   // pair group for the paired epilogues) with vector accesses.  acc[i][r] is tile row
   // 32 i + 8 (r / 4) + 4 (lane / 32) + r % 4, tile column 32 nw + lane % 32.
-  static_assert(32 * FM * 128 * 4 == (int)sizeof(As), "epilogue tile must fill the stage buffers");
+  constexpr int BN_ = 32 * NW;
+  static_assert(32 * FM * BN_ * 4 <= (int)sizeof(As), "epilogue tile must fit the stage buffers");
   float* T_ = (float*)&As[0][0];
   __syncthreads();  // every wave's last DMA has landed (vmcnt(0) above) and its LDS reads are done
   static_for<0, FM>([&](auto i) {
     static_for<0, 16>([&](auto r) {
       constexpr int R = decltype(r)::value;
       const int row = (int)decltype(i)::value * 32 + 8 * (R / 4) + 4 * (lane >> 5) + (R % 4);
-      T_[row * 128 + nw * 32 + (lane & 31)] = acc[i][R];
+      T_[row * BN_ + nw * 32 + (lane & 31)] = acc[i][R];
     });
   });
   __syncthreads();
   constexpr bool paired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
   constexpr int W = paired ? 16 : 8;        // columns per item
+  constexpr int BN = 32 * NW;               // tile columns
+  constexpr int ITEMS = 32 * FM * (BN / W);
+  const int m0 = mt * FM * 32, n0 = nt * BN;
+  for (int it = tid; it < ITEMS; it += 64 * NW) {
+    const int row = it / (BN / W), col = (it % (BN / W)) * W;
+    const int m = m0 + row, nc = n0 + col;
+    if (m >= a.M || nc >= a.N) continue;  // N % 16 == 0: a group is wholly inside or outside
+    float v[W];
+#pragma unroll
+    for (int e = 0; e < W; e += 4) *(f32x4*)&v[e] = *(const f32x4*)&T_[row * BN + col + e];
+    if (S > 1) {
+      float* dst = a.partial + ((size_t)sp * a.M + m) * a.N + nc;
+#pragma unroll
+      for (int e = 0; e < W; e += 4) *(f32x4*)(dst + e) = *(const f32x4*)&v[e];
+    } else if constexpr (paired) {
+      epi_group16<bf16, EPI>(a, m, nc, v, v + 8);
+    } else {
+      epi_group8<bf16, EPI>(a, m, nc, v);
+    }
+  }
+}
+
+// Two-column-block variant for FM >= 2: the four waves form 2 row groups x 2 column groups of
+// 64 columns (two 32-column weight blocks), so every activation fragment read from LDS feeds
+// two MFMAs and the LDS read traffic per flop halves.  Row group 0 takes the first
+// ceil(FM / 2) m-blocks, group 1 the rest.  Weights run two stages ahead (deeper rings measured
+// slower: more requests in flight only queue).  Waits and epilogue as in gemm32_kernel.
+template <int FM, int EPI>
+__global__ __launch_bounds__(256, 1) void gemm32x2_kernel(GemmArgs a) {
+  constexpr int KS = 4, NBUF = 4, PFB = 8, BLK = 512;
+  constexpr int SB = FM * KS;  // fragment blocks per stage
+  constexpr int D = SB / 4;    // DMAs per wave per stage
+  constexpr int P = PFB / KS;  // stages of weight lookahead
+  constexpr int MB0 = (FM + 1) / 2, MB1 = FM / 2;
+  static_assert(FM >= 2 && SB % 4 == 0 && (NBUF * KS) % PFB == 0 && P >= 1, "pipeline shape");
+  __shared__ __attribute__((aligned(1024))) bf16 As[NBUF][SB * BLK];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, rg = wave >> 1, cg = wave & 1;
+  const int n_blocks = (a.N + 31) >> 5, n_nt = (n_blocks + 3) / 4;
+  const int m_blocks = (a.M + 31) >> 5, n_mt = (m_blocks + FM - 1) / FM;
+  const int S = a.splits;
+  const int t = xcd_remap(blockIdx.x, n_mt * n_nt * S);
+  const int mt = t % n_mt, rest = t / n_mt;
+  const int sp = rest % S, nt = rest / S;
+  const int ks16 = a.Kp >> 4;
+  const int units = ks16 / (KS * NBUF), per = (units + S - 1) / S;
+  const int kb = min(units, sp * per) * (KS * NBUF), ke = min(units, sp * per + per) * (KS * NBUF);
+  const int n_st = (ke - kb) / KS;  // a multiple of NBUF
+  // this wave's two weight blocks (past N: a valid block whose columns are never stored)
+  const bf16* bp0 = (const bf16*)a.B + (size_t)min(nt * 4 + cg * 2, n_blocks - 1) * a.bstride + lane * 8;
+  const bf16* bp1 = (const bf16*)a.B + (size_t)min(nt * 4 + cg * 2 + 1, n_blocks - 1) * a.bstride + lane * 8;
+  const bf16* __restrict__ Ab = (const bf16*)a.A;
+
+  auto dma = [&](auto buf, int st) {
+    static_for<0, D>([&](auto d) {
+      const int q = wave + 4 * decltype(d)::value, mb = q / KS, j = q % KS;
+      const int k = min(kb + st * KS + j, ks16 - 1);
+      const int blk = min(mt * FM + mb, m_blocks - 1);  // rows past M: a valid block, never stored
+      const bf16* src = Ab + (size_t)blk * a.astride + (size_t)k * BLK + lane * 8;
+      __builtin_amdgcn_global_load_lds((const void*)src, (__attribute__((address_space(3))) void*)&As[buf][q * BLK],
+                                       16, 0, 0);
+    });
+  };
+  float* T_ = (float*)&As[0][0];
+  static_assert(32 * FM * 128 * 4 <= (int)sizeof(As), "epilogue tile must fit the stage buffers");
+
+  // The main loop for a row group of MB m-blocks starting at MOFF; ends with the group's
+  // accumulators parked in LDS as the fp32 tile [32 FM][128].
+  auto body = [&](auto mb_c, auto moff_c) {
+    constexpr int MB = decltype(mb_c)::value, MOFF = decltype(moff_c)::value;
+    bf16x8 rb[PFB][2];
+    auto load_b = [&](auto slot, int st, int j) {
+      const int k = min(kb + st * KS + j, ks16 - 1);
+      const bf16* s0 = bp0 + (size_t)k * BLK;
+      const bf16* s1 = bp1 + (size_t)k * BLK;
+      bf16x8 v0, v1;
+      asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v0) : "v"(s0) : "memory");
+      asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v1) : "v"(s1) : "memory");
+      rb[slot][0] = v0;
+      rb[slot][1] = v1;
+    };
+    f32x16 acc[MB][2];
+    static_for<0, MB>([&](auto i) {
+      acc[i][0] = f32x16{};
+      acc[i][1] = f32x16{};
+    });
+    static_for<0, NBUF - 1>([&](auto b) {
+      dma(b, b);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    static_for<0, P>([&](auto s) {
+      static_for<0, KS>([&](auto j) { load_b(std::integral_constant<int, s * KS + j>{}, s, j); });
+    });
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the loop's waits count from a full ring
+    __builtin_amdgcn_sched_barrier(0);
+
+    for (int st0 = 0; st0 < n_st; st0 += NBUF) {
+      static_for<0, NBUF>([&](auto u) {
+        constexpr int U = decltype(u)::value;
+        const int st = st0 + U;
+        // Stage st needs its weights (the last loads of stage st - P) and its activations (the
+        // DMA at the top of stage st - NBUF + 1); loads complete in order, so the wait counts
+        // what was issued after the later of the two.  Per stage: D DMAs, then 2 KS weight loads.
+        constexpr int WAIT = P <= NBUF - 1 ? (P - 1) * (D + 2 * KS) : 2 * KS + (NBUF - 2) * (D + 2 * KS);
+        static_assert(WAIT <= 63, "vmcnt range");
+        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(WAIT) : "memory");
+        dma(std::integral_constant<int, (U + NBUF - 1) % NBUF>{}, st + NBUF - 1);
+        __builtin_amdgcn_sched_barrier(0);
+        bf16x8 af[2][MB];
+        static_for<0, MB>([&](auto i) {
+          af[0][i] = *(const bf16x8*)(&As[U][((MOFF + decltype(i)::value) * KS) * BLK + lane * 8]);
+        });
+        static_for<0, KS>([&](auto j) {
+          constexpr int J = decltype(j)::value;
+          constexpr int slot = (U * KS + J) % PFB;
+          if constexpr (J + 1 < KS) {
+            static_for<0, MB>([&](auto i) {
+              af[(J + 1) & 1][i] =
+                  *(const bf16x8*)(&As[U][((MOFF + decltype(i)::value) * KS + J + 1) * BLK + lane * 8]);
+            });
+          }
+          __builtin_amdgcn_sched_barrier(0);
+          static_for<0, MB>([&](auto i) {
+            acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[J & 1][i], rb[slot][0], acc[i][0], 0, 0, 0);
+            acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[J & 1][i], rb[slot][1], acc[i][1], 0, 0, 0);
+          });
+          load_b(std::integral_constant<int, slot>{}, st + P, J);
+          __builtin_amdgcn_sched_barrier(0);
+        });
+      });
+    }
+    // The ring's last (unused) loads land before any of its registers can be reused.
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+#pragma unroll
+    for (int p = 0; p < PFB; ++p) {
+      asm volatile("" : "+v"(rb[p][0]));
+      asm volatile("" : "+v"(rb[p][1]));
+    }
+    __syncthreads();  // every wave's DMAs have landed and its LDS reads are done
+    static_for<0, MB>([&](auto i) {
+      static_for<0, 2>([&](auto n) {
+        static_for<0, 16>([&](auto r) {
+          constexpr int R = decltype(r)::value;
+          const int row = (MOFF + (int)decltype(i)::value) * 32 + 8 * (R / 4) + 4 * (lane >> 5) + (R % 4);
+          T_[row * 128 + cg * 64 + (int)decltype(n)::value * 32 + (lane & 31)] = acc[i][n][R];
+        });
+      });
+    });
+  };
+  if (rg == 0)
+    body(std::integral_constant<int, MB0>{}, std::integral_constant<int, 0>{});
+  else
+    body(std::integral_constant<int, MB1>{}, std::integral_constant<int, MB0>{});
+  __syncthreads();
+
+  // ---------------- epilogue over the fp32 tile (as in gemm32_kernel)
+  constexpr bool paired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
+  constexpr int W = paired ? 16 : 8;
   constexpr int ITEMS = 32 * FM * (128 / W);
   const int m0 = mt * FM * 32, n0 = nt * 128;
   for (int it = tid; it < ITEMS; it += 256) {
@@ -578,46 +737,53 @@ static int fm_for(int M) {
   return mb <= 1 ? 1 : mb <= 3 ? 3 : 9;
 }
 
-template <int FM>
+template <int FM, bool X2>
 static hipError_t gemm32_launch(int epi, const GemmArgs& a, hipStream_t s) {
   const int n_nt = ((a.N + 31) / 32 + 3) / 4, n_mt = ((a.M + 31) / 32 + FM - 1) / FM;
   dim3 grid(n_mt * n_nt * a.splits), block(256);
+#define AF_GEMM32(E)                                                                 \
+  if constexpr (X2) hipLaunchKernelGGL((gemm32x2_kernel<FM, E>), grid, block, 0, s, a); \
+  else hipLaunchKernelGGL((gemm32_kernel<FM, 4, E>), grid, block, 0, s, a);
   switch (epi) {
-    case EPI_STORE: hipLaunchKernelGGL((gemm32_kernel<FM, EPI_STORE>), grid, block, 0, s, a); break;
-    case EPI_STORE_F32: hipLaunchKernelGGL((gemm32_kernel<FM, EPI_STORE_F32>), grid, block, 0, s, a); break;
-    case EPI_RESID: hipLaunchKernelGGL((gemm32_kernel<FM, EPI_RESID>), grid, block, 0, s, a); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((gemm32_kernel<FM, EPI_SWIGLU>), grid, block, 0, s, a); break;
-    case EPI_QKV: hipLaunchKernelGGL((gemm32_kernel<FM, EPI_QKV>), grid, block, 0, s, a); break;
+    case EPI_STORE: AF_GEMM32(EPI_STORE) break;
+    case EPI_STORE_F32: AF_GEMM32(EPI_STORE_F32) break;
+    case EPI_RESID: AF_GEMM32(EPI_RESID) break;
+    case EPI_SWIGLU: AF_GEMM32(EPI_SWIGLU) break;
+    case EPI_QKV: AF_GEMM32(EPI_QKV) break;
     default: return hipErrorInvalidValue;
   }
+#undef AF_GEMM32
   return hipGetLastError();
+}
+
+// Split-K factor for a given tile count: none when the tiles alone fill most of the 256 CUs,
+// else the largest factor (<= 8) that keeps every workgroup in one round, with at least one
+// unit (256 k) per split.
+static int splits_for(int tiles, int units) {
+  if (tiles >= 160) return 1;
+  return std::max(1, std::min(std::min(8, 256 / tiles), units));
 }
 
 static hipError_t gemm_dispatch_bf16(int epi, const GemmArgs& a, hipStream_t s) {
   if (a.astride <= 0 || a.Kp % 256 != 0 || a.astride < (long)a.Kp * 32 || a.bstride < (long)a.Kp * 32)
     return hipErrorInvalidValue;
   const int fm = fm_for(a.M);
-  hipError_t e = fm == 1 ? gemm32_launch<1>(epi, a, s) : fm == 3 ? gemm32_launch<3>(epi, a, s) : gemm32_launch<9>(epi, a, s);
+  const hipError_t e = fm == 1 ? gemm32_launch<1, false>(epi, a, s)
+                       : fm == 3 ? gemm32_launch<3, true>(epi, a, s) : gemm32_launch<9, true>(epi, a, s);
   if (e != hipSuccess || a.splits <= 1) return e;
   return reduce_launch<bf16>(epi, a, s);
 }
 
-// Split K only when the output tiles alone would leave most of the 256 CUs idle: then the
-// largest factor (<= 8 for bf16, 4 for fp32) that keeps all workgroups in one round, with at
-// least one whole unit of k steps per split.
 int gemm_splits(int dtype, int M, int N, int Kp) {
-  int tiles, cap;
   if (dtype == AF_BF16) {
     const int fm = fm_for(M);
-    tiles = (((M + 31) / 32 + fm - 1) / fm) * (((N + 31) / 32 + 3) / 4);
-    cap = 8;
-  } else {
-    const int bm = bm_for_f32(M);
-    tiles = ((M + bm - 1) / bm) * ((N + 127) / 128);
-    cap = 4;
+    const int tiles = (((M + 31) / 32 + fm - 1) / fm) * (((N + 31) / 32 + 3) / 4);
+    return splits_for(tiles, Kp / gemm_k_align());
   }
+  const int bm = bm_for_f32(M);
+  const int tiles = ((M + bm - 1) / bm) * ((N + 127) / 128);
   if (tiles >= 160) return 1;
-  return std::max(1, std::min(std::min(cap, 256 / tiles), Kp / gemm_k_align()));
+  return std::max(1, std::min(std::min(4, 256 / tiles), Kp / gemm_k_align()));
 }
 
 int gemm_k_align() { return 256; }
