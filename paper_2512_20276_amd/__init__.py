@@ -3,7 +3,7 @@
 Argument marshalling only: every step of the path runs in the library's HIP kernels.
 Device buffers are passed as torch tensors (their data pointers); PyTorch provides
 device memory and streams.  Importing this module loads the in-tree shared library and
-raises if it has not been built (``python -m paper_2512_20276_amd.build``); there is no
+raises if it has not been built (``python paper_2512_20276_amd/build.py``); there is no
 fallback implementation.
 """
 from __future__ import annotations
@@ -58,7 +58,7 @@ class Segment(C.Structure):
 
 def _load():
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2512_20276_amd.build` "
+        raise ImportError(f"{LIB_PATH} is not built; run `python paper_2512_20276_amd/build.py` "
                           "(the HIP library is required: there is no fallback)")
     lib = C.CDLL(LIB_PATH)
     P, I32, I64, U32, F32 = C.c_void_p, C.c_int32, C.c_int64, C.c_uint32, C.c_float
