@@ -829,14 +829,17 @@ __device__ __forceinline__ float dot_vec(const uint4& k, const uint4& q, float a
 }
 
 template <typename T, int HD>
-__global__ __launch_bounds__(256) void attention_decode_kernel(AttnArgs a) {
+__device__ __forceinline__ void attention_decode_row(const AttnArgs& a, int tile) {
   constexpr int VEC = Chunk<T>::N;  // elements per 16 bytes
-  constexpr int DG = HD / VEC;      // dim groups
-  constexpr int KG = 64 / DG;       // key groups per 64-key chunk
-  static_assert(DG <= 64 && 64 % DG == 0, "head_dim");
+  constexpr int DG = HD / VEC;      // 16-byte chunks per key row
+  constexpr int KH2 = DG / 2;       // chunks per half row (two lanes per key for the scores)
+  constexpr int KG = 64 / DG;       // value key groups (lane / DG)
+  constexpr int KPL = 32 / KG;      // values: keys per lane per 32-key chunk
+  static_assert(DG % 2 == 0 && DG <= 64 && 64 % DG == 0 && 32 % KG == 0, "head_dim");
   __shared__ float wm[4], wl[4];
   __shared__ __attribute__((aligned(16))) float wo[4][HD];
-  const int seg_i = a.tiles[2 * (a.n_multi + blockIdx.x)];
+  __shared__ __attribute__((aligned(16))) uint4 qs[DG];
+  const int seg_i = a.tiles[2 * tile];
   const int h = blockIdx.y;
   const DevSeg sg = a.segs[seg_i];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -844,35 +847,36 @@ __global__ __launch_bounds__(256) void attention_decode_kernel(AttnArgs a) {
   const size_t slot_off = ((size_t)sg.slot * a.n_heads + h) * a.max_pos * HD;
   const T* __restrict__ Kg = (const T*)a.ring_k + slot_off;
   const T* __restrict__ Vg = (const T*)a.ring_v + slot_off;
-  const uint4* qrow = (const uint4*)((const T*)a.q + (size_t)sg.q_start * a.ldq + h * HD);
-  uint4 qv[DG];  // the query, the same in every lane
-#pragma unroll
-  for (int pc = 0; pc < DG; ++pc) qv[pc] = qrow[pc];
+  // the query, the same for every lane, is read from LDS (broadcast reads)
+  if (tid < DG) qs[tid] = ((const uint4*)((const T*)a.q + (size_t)sg.q_start * a.ldq + h * HD))[tid];
+  __syncthreads();
 
-  const int dg = lane % DG, kgrp = lane / DG;
+  const int half = lane & 1, kl = lane >> 1;   // scores: key kl of the chunk, half row `half`
+  const int dg = lane % DG, kgrp = lane / DG;  // values: dims [VEC dg, +VEC) of keys kgrp + KG t
   float m_run = -INFINITY, l_run = 0.f, o[VEC];
 #pragma unroll
   for (int e = 0; e < VEC; ++e) o[e] = 0.f;
-  for (int c = wave; c * 64 < kv_len; c += 4) {
-    // lane l scores key c*64 + l; past kv_len it reads a clamped valid key and scores -inf
-    const int j = c * 64 + lane;
-    const uint4* krow = (const uint4*)(Kg + (size_t)min(j, kv_len - 1) * HD);
-    uint4 kv[DG], vv[64 / KG];
+  for (int c = wave; c * 32 < kv_len; c += 4) {
+    // keys past kv_len read a clamped valid key and score -inf
+    const int j = c * 32 + kl;
+    const uint4* krow = (const uint4*)(Kg + (size_t)min(j, kv_len - 1) * HD) + half * KH2;
+    uint4 kv[KH2], vv[KPL];
 #pragma unroll
-    for (int pc = 0; pc < DG; ++pc) kv[pc] = krow[pc];
+    for (int pc = 0; pc < KH2; ++pc) kv[pc] = krow[pc];
 #pragma unroll
-    for (int t = 0; t < 64 / KG; ++t)
-      vv[t] = *(const uint4*)(Vg + (size_t)min(c * 64 + kgrp + KG * t, kv_len - 1) * HD + dg * VEC);
+    for (int t = 0; t < KPL; ++t)
+      vv[t] = *(const uint4*)(Vg + (size_t)min(c * 32 + kgrp + KG * t, kv_len - 1) * HD + dg * VEC);
     float dot = 0.f;
 #pragma unroll
-    for (int pc = 0; pc < DG; ++pc) dot = dot_vec<T>(kv[pc], qv[pc], dot);
+    for (int pc = 0; pc < KH2; ++pc) dot = dot_vec<T>(kv[pc], qs[half * KH2 + pc], dot);
+    dot += __shfl_xor(dot, 1);
     const float sc = j < kv_len ? dot * a.scale_log2 : -INFINITY;
     float cm = sc;
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) cm = fmaxf(cm, __shfl_xor(cm, off));
+    for (int off = 32; off > 1; off >>= 1) cm = fmaxf(cm, __shfl_xor(cm, off));
     const float m_new = fmaxf(m_run, cm);
     const float p = exp2f(sc - m_new);
-    float ps = p;
+    float ps = half ? 0.f : p;  // each key is held by two lanes
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) ps += __shfl_xor(ps, off);
     const float corr = exp2f(m_run - m_new);  // 0 on the first chunk (m_run = -inf)
@@ -880,10 +884,10 @@ __global__ __launch_bounds__(256) void attention_decode_kernel(AttnArgs a) {
     m_run = m_new;
 #pragma unroll
     for (int e = 0; e < VEC; ++e) o[e] *= corr;
-    // lane covers dims [VEC dg, +VEC) of keys c*64 + kgrp + KG t (masked keys carry p = 0)
+    // lane covers dims [VEC dg, +VEC) of keys c*32 + kgrp + KG t (masked keys carry p = 0)
 #pragma unroll
-    for (int t = 0; t < 64 / KG; ++t) {
-      const float pj = __shfl(p, kgrp + KG * t);
+    for (int t = 0; t < KPL; ++t) {
+      const float pj = __shfl(p, 2 * (kgrp + KG * t));
       T vt[VEC];
       __builtin_memcpy(vt, &vv[t], 16);
 #pragma unroll
@@ -925,13 +929,18 @@ __global__ __launch_bounds__(256) void attention_decode_kernel(AttnArgs a) {
   }
 }
 
+// Query tiles of multi-row segments.  The next key/value tile is loaded into registers while
+// the current one is processed from LDS (one memory latency per segment, not per tile).
 template <typename T, int HD>
-__global__ __launch_bounds__(256) void attention_kernel(AttnArgs a) {
+__device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int tile) {
   constexpr int VEC = Chunk<T>::N;
   constexpr int KROW = HD + VEC;            // padded key row (elements)
   constexpr int VROW = ATTN_BKV + VEC;      // padded transposed-value row
   constexpr int KST = HD / 32;              // MFMA k steps over the head dimension
   constexpr int DB = HD / 16;               // 16-dim output blocks
+  constexpr int CPR = HD / VEC;             // 16-byte chunks per key row
+  constexpr int NCH = ATTN_BKV * CPR / 256; // chunks of K (and of V) per thread per tile
+  static_assert((ATTN_BKV * CPR) % 256 == 0, "tile shape");
   typedef typename Mma<T>::frag frag;
 
   __shared__ __attribute__((aligned(16))) T Ks[ATTN_BKV * KROW];
@@ -939,7 +948,7 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
-  const int seg_i = a.tiles[2 * blockIdx.x], i0 = a.tiles[2 * blockIdx.x + 1];
+  const int seg_i = a.tiles[2 * tile], i0 = a.tiles[2 * tile + 1];
   const int h = blockIdx.y;
   const DevSeg sg = a.segs[seg_i];
   const int rows_here = min(ATTN_BQ, sg.q_len - i0);
@@ -968,26 +977,57 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a) {
   for (int d = 0; d < DB; ++d) oacc[d] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
 
+  // One tile's keys and values in registers.  Keys: thread t holds 16-byte chunk t % CPR of
+  // keys t / CPR + KR j (row-major LDS writes, one key row per CPR lanes).  Values: thread t
+  // holds KPT consecutive keys (t % KGV) * KPT .. of dim chunk t / KGV, so that after a
+  // transpose in registers each dim's KPT keys go to LDS as one contiguous write.
+  constexpr int KR = 256 / CPR;          // key rows per pass
+  constexpr int KPT = NCH;               // values: keys per thread
+  constexpr int KGV = ATTN_BKV / KPT;    // values: key groups
+  static_assert(KGV * CPR == 256, "value mapping");
+  uint4 kreg[NCH], vreg[NCH];
+  const int kc = tid % CPR, kr = tid / CPR;
+  const int vg = tid % KGV, vc = tid / KGV;
+  auto load_tile = [&](int kb0) {
+#pragma unroll
+    for (int j = 0; j < NCH; ++j) {
+      const int key = kb0 + kr + KR * j;
+      kreg[j] = key < kv_end ? *(const uint4*)(Kg + (size_t)key * HD + kc * VEC) : zero4();
+      const int vkey = kb0 + vg * KPT + j;
+      vreg[j] = vkey < kv_end ? *(const uint4*)(Vg + (size_t)vkey * HD + vc * VEC) : zero4();
+    }
+  };
   const int n_kt = (kv_end + ATTN_BKV - 1) / ATTN_BKV;
+  load_tile(0);
   for (int kt = 0; kt < n_kt; ++kt) {
     const int kb0 = kt * ATTN_BKV;
-    // ---- stage keys [kb0, kb0+64) (row-major) and values (transposed) of this slot and head
-    constexpr int CPR = HD / VEC;  // chunks per key row
-    for (int ci = tid; ci < ATTN_BKV * CPR; ci += 256) {
-      const int r = ci / CPR, c = ci % CPR;
-      const int key = kb0 + r;
-      uint4 kv4 = zero4(), vv4 = zero4();
-      if (key < kv_end) {
-        kv4 = *(const uint4*)(Kg + (size_t)key * HD + c * VEC);
-        vv4 = *(const uint4*)(Vg + (size_t)key * HD + c * VEC);
-      }
-      *(uint4*)(&Ks[r * KROW + c * VEC]) = kv4;
-      T vv[VEC];
-      __builtin_memcpy(vv, &vv4, 16);
+    // ---- park the tile in LDS: keys row-major, values transposed
+    __syncthreads();  // the previous tile's LDS reads are done
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) Vt[(c * VEC + e) * VROW + r] = vv[e];
+    for (int j = 0; j < NCH; ++j) *(uint4*)(&Ks[(kr + KR * j) * KROW + kc * VEC]) = kreg[j];
+    {
+      T vt[NCH][VEC];
+#pragma unroll
+      for (int j = 0; j < NCH; ++j) __builtin_memcpy(vt[j], &vreg[j], 16);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        T col[KPT];
+#pragma unroll
+        for (int j = 0; j < KPT; ++j) col[j] = vt[j][e];
+        T* dst = &Vt[(vc * VEC + e) * VROW + vg * KPT];
+        if constexpr (KPT * sizeof(T) == 4) {
+          *(unsigned*)dst = *(const unsigned*)col;
+        } else if constexpr (KPT * sizeof(T) == 8) {
+          *(uint2*)dst = *(const uint2*)col;
+        } else {
+          static_assert((KPT * sizeof(T)) % 16 == 0, "value chunk");
+#pragma unroll
+          for (int q = 0; q < (int)(KPT * sizeof(T)) / 16; ++q) *(uint4*)(dst + q * 16 / sizeof(T)) = *(const uint4*)(col + q * 16 / sizeof(T));
+        }
+      }
     }
     __syncthreads();
+    if (kt + 1 < n_kt) load_tile(kb0 + ATTN_BKV);  // in flight while this tile is processed
 
     if (wave_rows > 0 && kb0 <= wave_last_pos) {
       // ---- S^T = K . Q^T for 4 blocks of 16 keys
@@ -1040,19 +1080,30 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a) {
         }
 #pragma unroll
         for (int d = 0; d < DB; ++d) {
+          // keys lg * 4 .. +3 and 16 + lg * 4 .. +3 of the chunk: two aligned 4-element reads
           const T* vrow = &Vt[(d * 16 + lr) * VROW + c * 32 + lg * 4];
           frag vf;
+          if constexpr (sizeof(T) == 2) {
+            typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4_;
+            const bf16x4_ lo = *(const bf16x4_*)vrow, hi = *(const bf16x4_*)(vrow + 16);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            vf[e] = vrow[e];
-            vf[4 + e] = vrow[16 + e];
+            for (int e = 0; e < 4; ++e) {
+              vf[e] = lo[e];
+              vf[4 + e] = hi[e];
+            }
+          } else {
+            const f32x4 lo = *(const f32x4*)vrow, hi = *(const f32x4*)(vrow + 16);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              vf[e] = lo[e];
+              vf[4 + e] = hi[e];
+            }
           }
           oacc[d] = Mma<T>::mma(vf, pf, oacc[d]);
           if constexpr (sizeof(T) == 2) oacc[d] = Mma<T>::mma(vf, pf_lo, oacc[d]);
         }
       }
     }
-    __syncthreads();
   }
 
   if (wave_rows <= 0 || !q_ok) return;
@@ -1076,12 +1127,25 @@ __global__ __launch_bounds__(256) void attention_kernel(AttnArgs a) {
   }
 }
 
+// One launch for the whole step: work tiles [0, n_multi) are query tiles of multi-row segments
+// (ordered longest first, so they start first), the rest single-row segments.
+template <typename T, int HD, bool PREFILL>
+__global__ __launch_bounds__(256, PREFILL ? 3 : 4) void attention_kernel(AttnArgs a) {
+  if constexpr (PREFILL) {
+    if ((int)blockIdx.x < a.n_multi) {
+      attention_prefill_tile<T, HD>(a, blockIdx.x);
+      return;
+    }
+  }
+  attention_decode_row<T, HD>(a, blockIdx.x);
+}
+
 template <typename T, int HD>
 static void attention_launch(const AttnArgs& a, int n_tiles, hipStream_t s) {
   if (a.n_multi > 0)
-    hipLaunchKernelGGL((attention_kernel<T, HD>), dim3(a.n_multi, a.n_heads), dim3(256), 0, s, a);
-  if (n_tiles > a.n_multi)
-    hipLaunchKernelGGL((attention_decode_kernel<T, HD>), dim3(n_tiles - a.n_multi, a.n_heads), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((attention_kernel<T, HD, true>), dim3(n_tiles, a.n_heads), dim3(256), 0, s, a);
+  else  // decode rows only: without the prefill path's LDS and registers
+    hipLaunchKernelGGL((attention_kernel<T, HD, false>), dim3(n_tiles, a.n_heads), dim3(256), 0, s, a);
 }
 
 // tiles[0, n_multi) are query tiles of multi-row segments, tiles[n_multi, n_tiles) the
