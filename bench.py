@@ -245,6 +245,120 @@ def decode_heavy_attention(af, w, shape, n_pipe=8, K=8, L_P=276, reps=10):
     return out
 
 
+def _reserve(af, ring, specs):
+    """Ring reservation of one packed step: specs (request_id, pos0, q_len) in packing order; a
+    request not yet resident first gets pos0 positions of history.  Returns segment tuples."""
+    segs, row = [], 0
+    for rid, pos0, q_len in specs:
+        if pos0 > 0:
+            ring.append(rid, pos0)
+        s = ring.append(rid, q_len)
+        segs.append((row, q_len, s.slot, s.pos0, rid, af.AF_SEG_EMIT))
+        row += q_len
+    return segs
+
+
+def layer_roofline(M, D, F):
+    """Algorithmic GEMM flops and weight bytes of one layer at M rows (bf16 weights)."""
+    flops = 2 * M * (4 * D * D + 3 * D * F)
+    wbytes = 2 * (4 * D * D + 3 * D * F)
+    return flops, wbytes
+
+
+def sweep(af, w, shape, reps=4, n_layers=4):
+    """The packed-mix sweep: one layer forward per point (a prefill of P rows + d decode rows
+    with contexts uniform in {max(1, P), .., P + 7}; ring 16 slots x 544 with N(0, 1) history),
+    timed per kernel class with HIP events.  Successive runs rotate over n_layers weight layers
+    (1.6 GB for 4), so the 256 MB last-level cache does not hold the weights between runs."""
+    import torch
+    import workload as wl
+    H, hd, D, F = shape.n_heads, shape.head_dim, shape.d_model, shape.d_ff
+    n_slots, max_pos = wl.SWEEP_RING
+    ring = af.Ring(n_layers, n_slots, max_pos, H, hd, dtype=torch.bfloat16)
+    for l in range(n_layers):
+        kv = wl.draw(("sweep ring", l), (2, n_slots, max_pos, H, hd), device="cuda")
+        for sl in range(n_slots):
+            ring.write_kv(l, sl, 0, kv[0, sl], kv[1, sl])
+    del kv
+    points = []
+    for P in wl.SWEEP_PREFILL:
+        for d in wl.SWEEP_DECODE:
+            specs = wl.sweep_point_specs(P, d)
+            segs = _reserve(af, ring, specs)
+            M = sum(sg[1] for sg in segs)
+            x = wl.draw(("sweep rows", P, d), (M, D), device="cuda")
+            xs = [x.clone() for _ in range(n_layers)]
+            for l in range(n_layers):
+                af.packed_layer_forward(w, l, xs[l], segs, ring)
+            torch.cuda.synchronize()
+            w.timing_enable((1 << af.AF_K_COUNT) - 1)
+            for _ in range(reps):
+                for l in range(n_layers):
+                    af.packed_layer_forward(w, l, xs[l], segs, ring)
+            torch.cuda.synchronize()
+            tm = w.timing_read()
+            w.timing_enable(0)
+            n = reps * n_layers
+            gemm_us = sum(tm[k][0] for k in ("gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down")) / n * 1e3
+            at_us = tm["attention"][0] / n * 1e3
+            norm_us = tm["rmsnorm"][0] / n * 1e3
+            flops, wbytes = layer_roofline(M, D, F)
+            at_bytes = attention_bytes(segs, H, hd)
+            points.append({"P": P, "d": d, "M": M, "gemm_us": round(gemm_us, 2), "attention_us": round(at_us, 2),
+                           "rmsnorm_us": round(norm_us, 2),
+                           "gemm_frac_mfma": round(flops / (gemm_us * 1e-6) / (PEAK_BF16_TFLOPS * 1e12), 4),
+                           "gemm_frac_hbm": round(wbytes / (gemm_us * 1e-6) / (PEAK_HBM_GBS * 1e9), 4),
+                           "attention_frac_hbm": round(at_bytes / (at_us * 1e-6) / (PEAK_HBM_GBS * 1e9), 4)})
+            for sg in segs:
+                ring.release(sg[4])
+    ring.close()
+    return points
+
+
+def stress(af, w, shape, steps=8):
+    """The multi-pipeline stress workload: 8 pipelines of depth 8 (276-row prefill + 7 decode
+    rows each) packed into every 32-layer forward, M = 2264 rows in steady state, ring 64 slots x
+    288.  Warm-up until every step is full, then `steps` timed steps and a per-kernel pass."""
+    import torch
+    import workload as wl
+    from paper_2512_20276_amd.pipeline import Pipeline
+    st = wl.STRESS
+    P, K, L_V, L_T = st["n_pipes"], st["K"], st["n_vision"], st["n_text"]
+    L_P, D, F = L_V + L_T, shape.d_model, shape.d_ff
+    ring = af.Ring(shape.n_layers, st["n_slots"], st["max_pos"], shape.n_heads, shape.head_dim, dtype=torch.bfloat16)
+    text = wl.draw_ids(("instruction", 0), L_T, shape.vocab, device="cuda")
+    pids = torch.cat([torch.full((L_V,), -1, dtype=torch.int32, device="cuda"), text])
+    pool = []
+    for i in range(4):   # four distinct sets of camera frames, reused cyclically
+        e = torch.zeros((P * (L_P + K - 1), D), dtype=torch.bfloat16, device="cuda")
+        for p in range(P):
+            e[p * L_P:p * L_P + L_V] = wl.draw(("stress vision", i, p), (L_V, D), device="cuda")
+        pool.append(e)
+    pipe = Pipeline(w, ring, K, pids, lambda t: pool[t % len(pool)], keep_history=False, n_pipes=P)
+    for _ in range(K):
+        pipe.step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        M = pipe.step().M
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / steps
+    w.timing_enable((1 << af.AF_K_COUNT) - 1)
+    for _ in range(steps):
+        pipe.step()
+    torch.cuda.synchronize()
+    tm = w.timing_read()
+    w.timing_enable(0)
+    ring.close()
+    flops, _ = layer_roofline(M, D, F)
+    gemm_s = sum(tm[k][0] for k in ("gemm_qkv", "gemm_o", "gemm_gateup", "gemm_down")) / steps * 1e-3
+    return {"M": M, "pipelines": P, "K": K, "ms_per_step": round(dt * 1e3, 3),
+            "packed_steps_per_s": round(1 / dt, 3), "packed_tokens_per_s": round(M / dt, 1),
+            "action_tokens_per_s": round(P * K / dt, 1),
+            "mfma_frac_projection_gemms": round(flops * shape.n_layers / gemm_s / (PEAK_BF16_TFLOPS * 1e12), 4),
+            "kernel_ms_per_step": {k: round(ms / steps, 4) for k, (ms, n) in tm.items()}}
+
+
 # ----------------------------------------------------------------------------- cpu baseline
 def cpu_baseline(seconds_budget: float):
     """The oracle (float64 NumPy, as it stands) on a bounded sample of the same workload: one
@@ -423,6 +537,10 @@ def main():
                     "pipeline completes one request per step"}
         log("decode-heavy attention (8 pipelines x (276 + 7), 64 slots)")
         out["attention_stress"] = decode_heavy_attention(af, w, shape)
+        log("packed-mix sweep (one layer, 16 points)")
+        out["sweep"] = sweep(af, w, shape)
+        log("stress workload (8 pipelines, M = 2264, 32 layers)")
+        out["stress"] = stress(af, w, shape)
     ring.close()
     w.close()
     torch.cuda.empty_cache()

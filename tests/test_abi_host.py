@@ -133,3 +133,43 @@ def test_ring_create_rejects_bad_descriptors():
         with pytest.raises(af.AFError) as e:
             af.Ring(*args)
         assert e.value.code == af.AF_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("P,K,n_slots", [(8, 8, 64), (3, 4, 12), (2, 7, 16), (1, 7, 8)])
+def test_multi_pipeline_bookkeeping_matches_oracle_and_closed_form(P, K, n_slots):
+    """The pipeline driver's slot bookkeeping for P pipelines packed into one forward (stage-
+    major rows, request ids t * P + p), on a bookkeeping-only ring: every segment equals the
+    oracle RingModel's answer for the same calls, request r lives in slot r mod n_slots, and
+    its stage-s decode row sits at pos0 = L_P + s - 1 (kv_len = L_P + s)."""
+    import types
+
+    import torch
+
+    from paper_2512_20276_amd.pipeline import Pipeline
+
+    L_P = 276
+    ring = af.Ring(0, n_slots, 288)
+    model = RingModel(n_slots, 288)
+    shape = types.SimpleNamespace(d_model=8, vocab=4)
+    w = types.SimpleNamespace(shape=shape, dtype=torch.float32)
+    pipe = Pipeline(w, ring, K, torch.full((L_P,), -1, dtype=torch.int32), lambda t: None, n_pipes=P)
+    for t in range(3 * K + 2):
+        segs, M = pipe.reserve(t)
+        live = min(t + 1, K)
+        assert M == P * L_P + P * (live - 1)
+        row = 0
+        for i, s in enumerate(segs):
+            stage, p = divmod(i, P)
+            r = (t - stage) * P + p
+            n = L_P if stage == 0 else 1
+            assert (s.request_id, s.q_start, s.q_len) == (r, row, n)
+            assert (s.slot, s.pos0) == model.append(r, n)
+            assert s.slot == r % n_slots
+            assert s.pos0 == (0 if stage == 0 else L_P + stage - 1)
+            row += n
+        done = pipe.finish(segs)
+        assert sorted(done) == ([(t - K + 1) * P + p for p in range(P)] if t >= K - 1 else [])
+        for rid in done:
+            model.release(rid)
+        assert ring.state() == model.state()
+    ring.close()

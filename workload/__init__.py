@@ -27,7 +27,8 @@ import torch
 __all__ = [
     "ModelShape", "TINY", "LLAMA7B", "draw", "draw_ids", "layer_weights",
     "global_weights", "model_weights", "SegmentSpec", "pipeline_prefill_inputs",
-    "WEIGHT_STD", "LAYER_TENSORS",
+    "WEIGHT_STD", "LAYER_TENSORS", "SWEEP_PREFILL", "SWEEP_DECODE", "SWEEP_RING", "sweep_point_specs",
+    "STRESS",
 ]
 
 WEIGHT_STD = 0.02  # linear and embedding weights ~ N(0, 0.02)
@@ -160,3 +161,30 @@ def pipeline_prefill_inputs(shape: ModelShape, request: int, n_vision: int, text
     if n_text:
         ids[n_vision:] = text_ids.to(device=device, dtype=torch.int32)
     return ids, emb
+
+
+# ----------------------------------------------------------------------------- packed-mix sweep
+# One 7B-shape layer over every combination of a prefill of P rows and d single decode rows;
+# ring of 16 slots x 544 positions with N(0, 1) history.
+SWEEP_PREFILL = (0, 128, 276, 512)
+SWEEP_DECODE = (1, 3, 7, 15)
+SWEEP_RING = (16, 544)
+
+
+def sweep_point_specs(P: int, d: int, seed: int = 0) -> List[Tuple[int, int, int]]:
+    """(request_id, pos0, q_len) in packing order for sweep point (P, d): the prefill (if any)
+    as request 100 at positions 0..P-1, then decode rows of requests 200..200+d-1 whose context
+    (kv_len, the new row included) is uniform in {max(1, P), .., P + 7}."""
+    g = torch.Generator()
+    g.manual_seed(_seed(("sweep kv_len", seed, P, d)))
+    lo, hi = max(1, P), P + 7
+    kv = torch.randint(lo, hi + 1, (d,), generator=g).tolist()
+    specs = [(100, 0, P)] if P > 0 else []
+    return specs + [(200 + i, kv[i] - 1, 1) for i in range(d)]
+
+
+# ----------------------------------------------------------------------------- stress workload
+# Eight independent pipelines of depth 8 (a prefill of 256 vision + 20 instruction rows and the
+# decode rows of stages 1..7) packed into each forward of the 32-layer 7B shape: M = 8 x 283 =
+# 2264 rows in steady state, one ring slot per live request (64 slots x 288 positions).
+STRESS = dict(n_pipes=8, K=8, n_vision=256, n_text=20, n_slots=64, max_pos=288)
