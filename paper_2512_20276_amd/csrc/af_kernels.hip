@@ -732,9 +732,15 @@ __global__ __launch_bounds__(256, 1) void gemm32x2_kernel(GemmArgs a) {
   }
 }
 
+// 32-row blocks per tile: the smallest tile that holds every row (up to 10 blocks, 320 rows;
+// FM = 10 fills the 160 KB of LDS), else the tile of 9 or 10 blocks with the fewest tiles and
+// then the least padding.  A row's accumulation order is the same in every tile shape.
 static int fm_for(int M) {
   const int mb = (M + 31) / 32;
-  return mb <= 1 ? 1 : mb <= 3 ? 3 : 9;
+  for (int fm : {1, 3, 5, 7, 9, 10})
+    if (mb <= fm) return fm;
+  const int t9 = (mb + 8) / 9, t10 = (mb + 9) / 10;
+  return t10 < t9 || (t10 == t9 && t10 * 10 < t9 * 9) ? 10 : 9;
 }
 
 template <int FM, bool X2>
@@ -767,9 +773,15 @@ static int splits_for(int tiles, int units) {
 static hipError_t gemm_dispatch_bf16(int epi, const GemmArgs& a, hipStream_t s) {
   if (a.astride <= 0 || a.Kp % 256 != 0 || a.astride < (long)a.Kp * 32 || a.bstride < (long)a.Kp * 32)
     return hipErrorInvalidValue;
-  const int fm = fm_for(a.M);
-  const hipError_t e = fm == 1 ? gemm32_launch<1, false>(epi, a, s)
-                       : fm == 3 ? gemm32_launch<3, true>(epi, a, s) : gemm32_launch<9, true>(epi, a, s);
+  hipError_t e;
+  switch (fm_for(a.M)) {
+    case 1: e = gemm32_launch<1, false>(epi, a, s); break;
+    case 3: e = gemm32_launch<3, true>(epi, a, s); break;
+    case 5: e = gemm32_launch<5, true>(epi, a, s); break;
+    case 7: e = gemm32_launch<7, true>(epi, a, s); break;
+    case 9: e = gemm32_launch<9, true>(epi, a, s); break;
+    default: e = gemm32_launch<10, true>(epi, a, s); break;
+  }
   if (e != hipSuccess || a.splits <= 1) return e;
   return reduce_launch<bf16>(epi, a, s);
 }
@@ -1130,7 +1142,7 @@ __device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int ti
 // One launch for the whole step: work tiles [0, n_multi) are query tiles of multi-row segments
 // (ordered longest first, so they start first), the rest single-row segments.
 template <typename T, int HD, bool PREFILL>
-__global__ __launch_bounds__(256, PREFILL ? 3 : 4) void attention_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256, !PREFILL ? 4 : (sizeof(T) == 4 && HD == 128) ? 1 : 3) void attention_kernel(AttnArgs a) {
   if constexpr (PREFILL) {
     if ((int)blockIdx.x < a.n_multi) {
       attention_prefill_tile<T, HD>(a, blockIdx.x);
