@@ -52,6 +52,9 @@ def parse():
     p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                    help="print the traffic summary of two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE "
                         "counter_collection.csv files of a --copy-calibration run) and exit")
+    p.add_argument("--summarize-mfma", nargs=2, metavar=("COUNTER_CSV", "KERNEL_STATS_CSV"),
+                   help="print MFMA work per kernel class from a rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_BF16 "
+                        "SQ_VALU_MFMA_BUSY_CYCLES run and a --kernel-trace --stats run of the same command, and exit")
     p.add_argument("--summarize-stats", metavar="KERNEL_STATS_CSV",
                    help="print a per-kernel table of a rocprofv3 --kernel-trace --stats kernel_stats.csv and exit")
     return p.parse_args()
@@ -82,11 +85,13 @@ def measured_traffic():
 
 
 def _kernel_class(name: str) -> str:
-    """Maps a demangled kernel name to the label used in the summaries."""
+    """Maps a kernel name (mangled or demangled) to the label used in the summaries."""
     import re
-    if "gemm_kernel" in name:
-        epi = (re.search(r",\s*(\d)>\s*\(", name) or re.search(r",\s*\(af::Epi\)(\d)>", name)
-               or re.search(r"GemmCfgI(?:Li\d+E)+EELi(\d)E", name))   # demangled or mangled
+    if "gemm_kernel" in name or "gemm32_kernel" in name or "gemm32x2_kernel" in name:
+        epi = (re.search(r"gemm32(?:x2)?_kernelI(?:Li\d+E)*Li(\d+)EEEv", name)      # bf16, mangled
+               or re.search(r"gemm32(?:x2)?_kernel<[^>]*?(\d+)>", name)              # bf16, demangled
+               or re.search(r",\s*(\d)>\s*\(", name) or re.search(r",\s*\(af::Epi\)(\d)>", name)
+               or re.search(r"GemmCfgI(?:Li\d+E)+EELi(\d)E", name))                  # fp32 kernel
         e = int(epi.group(1)) if epi else -1
         return {0: "gemm (store)", 1: "gemm (f32 store, LM head)", 2: "gemm (+residual: O / down)",
                 3: "gemm (gate/up + SwiGLU)", 4: "gemm (QKV + RoPE + ring write)"}.get(e, "gemm")
@@ -143,6 +148,39 @@ def summarize_pmc(fetch_csv, write_csv):
         tb = int(round(f[g][0] * 1024 * fs + w[g][0] * 1024 * ws))
         print(f"\n- traffic_bytes_per_launch: {tb}")
         print(f"- kernel_source_sha256: `{kernels_sha256()}`")
+
+
+def summarize_mfma(counter_csv, stats_csv):
+    """MFMA work per kernel class from SQ_INSTS_VALU_MFMA_MOPS_BF16 (units of 512 flops) and
+    SQ_VALU_MFMA_BUSY_CYCLES (matrix-core cycles summed over every SIMD), against the average
+    duration of the same class in a --kernel-trace --stats run: busy fraction = busy cycles /
+    (duration x 2.4 GHz x 256 CUs x 4 SIMDs)."""
+    import csv
+    from collections import defaultdict
+    acc = defaultdict(lambda: defaultdict(lambda: [0.0, 0]))
+    for r in csv.DictReader(open(counter_csv)):
+        a = acc[_kernel_class(r["Kernel_Name"])][r["Counter_Name"]]
+        a[0] += float(r["Counter_Value"])
+        a[1] += 1
+    dur = defaultdict(lambda: [0.0, 0])
+    for r in csv.DictReader(open(stats_csv)):
+        d = dur[_kernel_class(r["Name"])]
+        d[0] += float(r["TotalDurationNs"])
+        d[1] += int(r["Calls"])
+    print("| kernel class | dispatches | MFMA GFLOP/dispatch (counter) | MFMA busy cycles/dispatch | avg us | "
+          "counter TFLOP/s | MFMA busy fraction |")
+    print("|---|---:|---:|---:|---:|---:|---:|")
+    for k, cs in sorted(acc.items(), key=lambda kv: -kv[1].get("SQ_VALU_MFMA_BUSY_CYCLES", [0, 1])[0]):
+        mops = cs.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", [0.0, 1])
+        busy = cs.get("SQ_VALU_MFMA_BUSY_CYCLES", [0.0, 1])
+        n = max(mops[1], 1)
+        fl = mops[0] / n * 512
+        bc = busy[0] / max(busy[1], 1)
+        if fl == 0 and bc == 0:
+            continue
+        us = dur[k][0] / dur[k][1] / 1e3 if dur[k][1] else float("nan")
+        print(f"| {k} | {n} | {fl / 1e9:.3f} | {bc:.4g} | {us:.2f} | {fl / (us * 1e-6) / 1e12:.1f} | "
+              f"{bc / (us * 1e-6 * 2.4e9 * 256 * 4):.4f} |")
 
 
 # ----------------------------------------------------------------------------- algorithmic work
@@ -417,6 +455,9 @@ def main():
         return
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc)
+        return
+    if args.summarize_mfma:
+        summarize_mfma(*args.summarize_mfma)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (each MI355X would run its "
