@@ -53,6 +53,7 @@ struct GemmArgs {
   long bstride;
   int splits;      // split-K factor (1 = none)
   float* partial;  // [splits][M][N] fp32 partial sums when splits > 1
+  int partials_only;  // with splits > 1: leave the sums and the epilogue to a later kernel
   void* out;       // EPI_STORE/_F32/_RESID: [M, N]; EPI_SWIGLU: [M, N/2]; EPI_QKV: queries [M, d_model]
   int ldo;
   long ostride;    // EPI_SWIGLU: > 0 writes the output fragment-tiled (32-row blocks ostride apart)
@@ -84,6 +85,11 @@ hipError_t launch_attention(int dtype, int head_dim, const AttnArgs& a, int n_ti
 // y row-major (row stride ldy) or, when ystride > 0, fragment-tiled.
 hipError_t launch_rmsnorm(int dtype, const void* x, int ldx, const int32_t* rows, const void* g, void* y, int ldy,
                           long ystride, int n_rows, int D, float eps, hipStream_t s);
+// Residual update from split-K partial sums followed by the RMSNorm of the updated rows:
+// x[m] <- x[m] + sum_s partial[s][m] (rounded as the residual epilogue rounds), then y[m] =
+// RMSNorm(x[m]) * g exactly as launch_rmsnorm computes it.  partial is [splits][M][D].
+hipError_t launch_resid_norm(int dtype, const float* partial, int splits, void* x, int ldx, const void* g, void* y,
+                             int ldy, long ystride, int M, int D, float eps, hipStream_t s);
 // Row-major [M, K] (row stride ld) -> fragment-tiled (32-row blocks astride apart), with the
 // rows of the last block past M and the columns [K, Kp) written as zeros.
 hipError_t launch_to_frag(int dtype, const void* x, int ld, int M, int K, int Kp, void* y, long astride,

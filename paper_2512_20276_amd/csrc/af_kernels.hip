@@ -423,7 +423,7 @@ static hipError_t gemm_dispatch_f32(int epi, const GemmArgs& a, hipStream_t s) {
   const int bm = bm_for_f32(a.M);
   hipError_t e = bm == 32 ? gemm_launch_cfg<float, CfgF32S>(epi, a, s)
                  : bm == 96 ? gemm_launch_cfg<float, CfgF32M>(epi, a, s) : gemm_launch_cfg<float, CfgF32L>(epi, a, s);
-  if (e != hipSuccess || a.splits <= 1) return e;
+  if (e != hipSuccess || a.splits <= 1 || a.partials_only) return e;
   return reduce_launch<float>(epi, a, s);
 }
 
@@ -782,7 +782,7 @@ static hipError_t gemm_dispatch_bf16(int epi, const GemmArgs& a, hipStream_t s) 
     case 9: e = gemm32_launch<9, true>(epi, a, s); break;
     default: e = gemm32_launch<10, true>(epi, a, s); break;
   }
-  if (e != hipSuccess || a.splits <= 1) return e;
+  if (e != hipSuccess || a.splits <= 1 || a.partials_only) return e;
   return reduce_launch<bf16>(epi, a, s);
 }
 
@@ -1239,6 +1239,98 @@ hipError_t launch_rmsnorm(int dtype, const void* x, int ldx, const int32_t* rows
   return hipGetLastError();
 }
 
+// Split-K sum + residual + RMSNorm, one workgroup per row.  Each thread covers the same
+// elements, in the same order, as splitk_reduce_kernel<EPI_RESID> followed by rmsnorm_kernel
+// would, so the residual row and the normalised row are bit-identical to that pair of launches
+// (one launch fewer, and the row is summed and normalised while it is on chip).
+template <typename T>
+__global__ __launch_bounds__(256) void resid_norm_kernel(const float* __restrict__ partial, int splits, T* x, int ldx,
+                                                         const T* __restrict__ g, T* __restrict__ y, int ldy,
+                                                         long ystride, int M, int D, float eps) {
+  __shared__ float red[4];
+  const int m = blockIdx.x;
+  T* xr = x + (size_t)m * ldx;
+  const size_t plane = (size_t)M * D;
+  constexpr int V = 16 / sizeof(T);
+  const bool vec = sizeof(T) == 2 && D % 8 == 0 && ldx % 8 == 0;
+  float ss = 0.f;
+  if (vec) {
+    for (int i = threadIdx.x * V; i < D; i += 256 * V) {
+      // all of this chunk's partial sums are requested before any is added (one memory latency
+      // instead of one per split); they are added in split order
+      constexpr int MAXS = 8;
+      float t[MAXS][8];
+#pragma unroll
+      for (int sp = 0; sp < MAXS; ++sp)
+        if (sp < splits) load8<float>(partial + sp * plane + (size_t)m * D + i, t[sp]);
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = 0.f;
+#pragma unroll
+      for (int sp = 0; sp < MAXS; ++sp)
+        if (sp < splits)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] += t[sp][e];
+      for (int sp = MAXS; sp < splits; ++sp) {
+        float u[8];
+        load8<float>(partial + sp * plane + (size_t)m * D + i, u);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] += u[e];
+      }
+      T res[8], r[8];
+      load8<T>(xr + i, res);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) r[e] = from_f<T>(to_f(res[e]) + v[e]);
+      store8<T>(xr + i, r);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss += to_f(r[e]) * to_f(r[e]);
+    }
+  } else {
+    for (int i = threadIdx.x; i < D; i += 256) {
+      float v = 0.f;
+      for (int sp = 0; sp < splits; ++sp) v += partial[sp * plane + (size_t)m * D + i];
+      const T r = from_f<T>(to_f(xr[i]) + v);
+      xr[i] = r;
+      ss += to_f(r) * to_f(r);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float tot = red[0] + red[1] + red[2] + red[3];
+  const float inv = 1.0f / sqrtf(tot / (float)D + eps);
+  if (vec) {  // each thread re-reads only the elements it wrote
+    for (int i = threadIdx.x * V; i < D; i += 256 * V) {
+      T v[V], gv[V], o[V];
+      *(uint4*)v = *(const uint4*)(xr + i);
+      *(uint4*)gv = *(const uint4*)(g + i);
+#pragma unroll
+      for (int e = 0; e < V; ++e) o[e] = from_f<T>(to_f(v[e]) * inv * to_f(gv[e]));
+      T* dst = ystride > 0 ? y + frag_off(m, i, ystride) : y + (size_t)m * ldy + i;
+      *(uint4*)dst = *(const uint4*)o;
+    }
+  } else {
+    for (int i = threadIdx.x; i < D; i += 256) {
+      const T o = from_f<T>(to_f(xr[i]) * inv * to_f(g[i]));
+      y[ystride > 0 ? frag_off(m, i, ystride) : (size_t)m * ldy + i] = o;
+    }
+  }
+}
+
+hipError_t launch_resid_norm(int dtype, const float* partial, int splits, void* x, int ldx, const void* g, void* y,
+                             int ldy, long ystride, int M, int D, float eps, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (splits < 1 || !partial) return hipErrorInvalidValue;
+  if (dtype == AF_BF16)
+    hipLaunchKernelGGL(resid_norm_kernel<bf16>, dim3(M), dim3(256), 0, s, partial, splits, (bf16*)x, ldx,
+                       (const bf16*)g, (bf16*)y, ldy, ystride, M, D, eps);
+  else
+    hipLaunchKernelGGL(resid_norm_kernel<float>, dim3(M), dim3(256), 0, s, partial, splits, (float*)x, ldx,
+                       (const float*)g, (float*)y, ldy, ystride, M, D, eps);
+  return hipGetLastError();
+}
+
 // Row-major -> fragment-tiled copy; one thread per 8 consecutive k of one row.
 __global__ __launch_bounds__(256) void to_frag_kernel(const bf16* __restrict__ x, int ld, int M, int K, int Kp,
                                                       bf16* __restrict__ y, long astride, int rows_padded) {
@@ -1290,16 +1382,29 @@ hipError_t launch_embed(int dtype, const int32_t* ids, const void* table, int vo
 }
 
 // ------------------------------------------------------------------ greedy argmax
-// One workgroup per row; the lowest index among equal maxima wins.
-__global__ __launch_bounds__(256) void argmax_kernel(const float* __restrict__ logits, int V, int32_t* tokens) {
-  __shared__ float sv[4];
-  __shared__ int si[4];
+// One workgroup of 1024 threads per row, 16-byte loads; the lowest index among equal maxima wins
+// (each thread scans its indices in increasing order and keeps the first maximum it meets; the
+// reduction prefers the lower index on equal values).
+__global__ __launch_bounds__(1024) void argmax_kernel(const float* __restrict__ logits, int V, int32_t* tokens) {
+  __shared__ float sv[16];
+  __shared__ int si[16];
   const float* z = logits + (size_t)blockIdx.x * V;
   float bv = -INFINITY;
   int bi = 0x7fffffff;
-  for (int i = threadIdx.x; i < V; i += 256) {
-    const float v = z[i];
-    if (v > bv) { bv = v; bi = i; }  // strided scan visits indices in increasing order
+  if (V % 4 == 0 && ((uintptr_t)z & 15) == 0) {
+    const float4* z4 = (const float4*)z;
+    for (int i = threadIdx.x; i < V / 4; i += 1024) {
+      const float4 v = z4[i];
+      if (v.x > bv) { bv = v.x; bi = 4 * i; }
+      if (v.y > bv) { bv = v.y; bi = 4 * i + 1; }
+      if (v.z > bv) { bv = v.z; bi = 4 * i + 2; }
+      if (v.w > bv) { bv = v.w; bi = 4 * i + 3; }
+    }
+  } else {
+    for (int i = threadIdx.x; i < V; i += 1024) {
+      const float v = z[i];
+      if (v > bv) { bv = v; bi = i; }
+    }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -1310,7 +1415,7 @@ __global__ __launch_bounds__(256) void argmax_kernel(const float* __restrict__ l
   if ((threadIdx.x & 63) == 0) { sv[threadIdx.x >> 6] = bv; si[threadIdx.x >> 6] = bi; }
   __syncthreads();
   if (threadIdx.x == 0) {
-    for (int w = 1; w < 4; ++w)
+    for (int w = 1; w < 16; ++w)
       if (sv[w] > bv || (sv[w] == bv && si[w] < bi)) { bv = sv[w]; bi = si[w]; }
     tokens[blockIdx.x] = bi == 0x7fffffff ? 0 : bi;
   }
@@ -1318,7 +1423,7 @@ __global__ __launch_bounds__(256) void argmax_kernel(const float* __restrict__ l
 
 hipError_t launch_argmax(const float* logits, int n_rows, int V, int32_t* tokens, hipStream_t s) {
   if (n_rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(argmax_kernel, dim3(n_rows), dim3(256), 0, s, logits, V, tokens);
+  hipLaunchKernelGGL(argmax_kernel, dim3(n_rows), dim3(1024), 0, s, logits, V, tokens);
   return hipGetLastError();
 }
 

@@ -491,13 +491,32 @@ af_status step_attention(af_weights* w, int dtype, af_ring* ring, int l, const v
   return timed(w, AF_K_ATTENTION, s, [&] { return launch_attention(dtype, ring->d.head_dim, a, t.n_tiles, s); });
 }
 
-af_status step_o(af_weights* w, int l, const void* o, int ldo_in, long os, void* hidden, int M, hipStream_t s) {
+// Residual projections (output and down).  With split-K and a norm gain, the partial sums, the
+// residual update and the RMSNorm of the updated rows (gain `norm`, into w->xn) run as one
+// kernel after the GEMM; *normed tells the caller whether that norm was produced.
+af_status step_resid_proj(af_weights* w, int cls, const void* A, int lda, long as, const void* W, int K, void* hidden,
+                          int M, const void* norm, bool* normed, hipStream_t s) {
   const af_model_desc& d = w->d;
-  GemmArgs g = gemm_args(d.dtype, o, ldo_in, os, w->layers[l].wo, M, d.d_model, d.d_model, hidden, d.d_model);
+  GemmArgs g = gemm_args(d.dtype, A, lda, as, W, M, d.d_model, K, hidden, d.d_model);
   g.resid = hidden;
   g.ldr = d.d_model;
   AF_TRY(with_splits(w, g));
-  return timed(w, AF_K_GEMM_O, s, [&] { return launch_gemm(d.dtype, EPI_RESID, g, s); });
+  *normed = norm && g.splits > 1;
+  if (!*normed) return timed(w, cls, s, [&] { return launch_gemm(d.dtype, EPI_RESID, g, s); });
+  g.partials_only = 1;
+  return timed(w, cls, s, [&] {
+    hipError_t e = launch_gemm(d.dtype, EPI_RESID, g, s);
+    if (e != hipSuccess) return e;
+    return launch_resid_norm(d.dtype, g.partial, g.splits, hidden, d.d_model, norm, w->xn, w->ldD, w->xs_D, M,
+                             d.d_model, d.rms_eps, s);
+  });
+}
+
+af_status step_o(af_weights* w, int l, const void* o, int ldo_in, long os, void* hidden, int M, hipStream_t s,
+                 const void* norm = nullptr, bool* normed = nullptr) {
+  bool dummy;
+  return step_resid_proj(w, AF_K_GEMM_O, o, ldo_in, os, w->layers[l].wo, w->d.d_model, hidden, M, norm,
+                         normed ? normed : &dummy, s);
 }
 
 af_status step_gate_up(af_weights* w, int l, const void* xn, int ldx, long xs, void* act, int ld_act, long act_os,
@@ -509,13 +528,11 @@ af_status step_gate_up(af_weights* w, int l, const void* xn, int ldx, long xs, v
   return timed(w, AF_K_GEMM_GATEUP, s, [&] { return launch_gemm(d.dtype, EPI_SWIGLU, g, s); });
 }
 
-af_status step_down(af_weights* w, int l, const void* act, int ld_act, long as, void* hidden, int M, hipStream_t s) {
-  const af_model_desc& d = w->d;
-  GemmArgs g = gemm_args(d.dtype, act, ld_act, as, w->layers[l].wdown, M, d.d_model, d.d_ff, hidden, d.d_model);
-  g.resid = hidden;
-  g.ldr = d.d_model;
-  AF_TRY(with_splits(w, g));
-  return timed(w, AF_K_GEMM_DOWN, s, [&] { return launch_gemm(d.dtype, EPI_RESID, g, s); });
+af_status step_down(af_weights* w, int l, const void* act, int ld_act, long as, void* hidden, int M, hipStream_t s,
+                    const void* norm = nullptr, bool* normed = nullptr) {
+  bool dummy;
+  return step_resid_proj(w, AF_K_GEMM_DOWN, act, ld_act, as, w->layers[l].wdown, w->d.d_ff, hidden, M, norm,
+                         normed ? normed : &dummy, s);
 }
 
 af_status step_norm(af_weights* w, const void* x, int ldx, const int32_t* rows, const void* g, void* y, int ldy,
@@ -526,18 +543,24 @@ af_status step_norm(af_weights* w, const void* x, int ldx, const int32_t* rows, 
   });
 }
 
-af_status layer_forward(af_weights* w, int l, void* hidden, int M, af_ring* ring, const DevTables& t, hipStream_t s) {
+// One decoder layer (Alg. 2).  xn_ready: the previous layer's down projection already wrote
+// this layer's attention-normed rows into w->xn.  next_norm: the next layer's attention-norm
+// gain, which this layer's down projection applies when it can (*next_ready then says so).
+af_status layer_forward(af_weights* w, int l, void* hidden, int M, af_ring* ring, const DevTables& t, hipStream_t s,
+                        bool xn_ready = false, const void* next_norm = nullptr, bool* next_ready = nullptr) {
   const Layer& L = w->layers[l];
   const int D = w->d.d_model, ldD = w->ldD, ldF = w->ldF;
   const long xD = w->xs_D, xF = w->xs_F;  // 0 (row-major) for fp32
-  AF_TRY(step_norm(w, hidden, D, nullptr, L.attn_norm, w->xn, ldD, xD, M, s));
+  if (!xn_ready) AF_TRY(step_norm(w, hidden, D, nullptr, L.attn_norm, w->xn, ldD, xD, M, s));
   AF_TRY(step_qkv(w, l, w->xn, ldD, xD, M, ring, t, w->q, ldD, s));
   AF_TRY(step_attention(w, w->d.dtype, ring, l, w->q, ldD, w->attn, ldD, xD, t, s));
   // InPlaceKVShift: no device work; the slot rotation lives in the ring bookkeeping.
-  AF_TRY(step_o(w, l, w->attn, ldD, xD, hidden, M, s));
-  AF_TRY(step_norm(w, hidden, D, nullptr, L.mlp_norm, w->xn, ldD, xD, M, s));
+  bool mlp_normed = false;
+  AF_TRY(step_o(w, l, w->attn, ldD, xD, hidden, M, s, L.mlp_norm, &mlp_normed));
+  if (!mlp_normed) AF_TRY(step_norm(w, hidden, D, nullptr, L.mlp_norm, w->xn, ldD, xD, M, s));
   AF_TRY(step_gate_up(w, l, w->xn, ldD, xD, w->act, ldF, xF, M, s));
-  AF_TRY(step_down(w, l, w->act, ldF, xF, hidden, M, s));
+  bool dummy;
+  AF_TRY(step_down(w, l, w->act, ldF, xF, hidden, M, s, next_norm, next_ready ? next_ready : &dummy));
   return AF_OK;
 }
 
@@ -749,7 +772,13 @@ extern "C" af_status af_packed_forward(af_weights* w, const int32_t* token_ids, 
   AF_TRY(timed(w, AF_K_EMBED, s, [&] {
     return launch_embed(d.dtype, token_ids, w->embed, d.vocab, embeds, out_hidden, M, d.d_model, w->dev_err, s);
   }));
-  for (int l = 0; l < d.n_layers; ++l) AF_TRY(layer_forward(w, l, out_hidden, M, ring, t, s));
+  bool xn_ready = false;
+  for (int l = 0; l < d.n_layers; ++l) {
+    const void* next = l + 1 < d.n_layers ? w->layers[l + 1].attn_norm : nullptr;
+    bool next_ready = false;
+    AF_TRY(layer_forward(w, l, out_hidden, M, ring, t, s, xn_ready, next, &next_ready));
+    xn_ready = next_ready;
+  }
   return lm_head(w, out_hidden, t, out_logits, out_tokens, s);
 }
 
