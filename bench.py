@@ -397,6 +397,42 @@ def stress(af, w, shape, steps=8):
             "kernel_ms_per_step": {k: round(ms / steps, 4) for k, (ms, n) in tm.items()}}
 
 
+def k_sweep(af, w, shape, pids, Ks=(7, 16, 24, 32), steps=12):
+    """Action length K swept as in the paper's K experiment: the 32-layer pipeline at each K
+    (one 276-row prefill + K - 1 decode rows per step, ring K + 1 slots), against the plain
+    per-request schedule on the same kernels (prefill, then K - 1 single-row decodes)."""
+    import torch
+    import workload as wl
+    from paper_2512_20276_amd.pipeline import Pipeline
+    L_P, D = int(pids.numel()), shape.d_model
+    L_V = int((pids < 0).sum().item())
+    out = []
+    for K in Ks:
+        max_pos = (L_P + K + 31) // 32 * 32
+        ring = af.Ring(shape.n_layers, K + 1, max_pos, shape.n_heads, shape.head_dim, dtype=torch.bfloat16)
+        pool = []
+        for i in range(4):
+            e = torch.zeros((L_P + K - 1, D), dtype=torch.bfloat16, device="cuda")
+            e[:L_V] = wl.draw(("vision", 0, i), (L_V, D), device="cuda")
+            pool.append(e)
+        pipe = Pipeline(w, ring, K, pids, lambda t: pool[t % len(pool)], keep_history=False)
+        for _ in range(K + 1):
+            pipe.step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            M = pipe.step().M
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / steps
+        ring.close()
+        seq_ms = sequential_baseline(af, w, shape, pids, pool, K, n_req=3, warm=1)
+        out.append({"K": K, "M": M, "ms_per_step": round(dt * 1e3, 3), "packed_steps_per_s": round(1 / dt, 2),
+                    "packed_tokens_per_s": round(M / dt, 1), "action_tokens_per_s": round(K / dt, 1),
+                    "sequential_ms_per_request": round(seq_ms, 3), "speedup_vs_sequential": round(seq_ms / (dt * 1e3), 3)})
+        log(f"K={K}: {dt * 1e3:.2f} ms/step, sequential {seq_ms:.2f} ms/request")
+    return out
+
+
 # ----------------------------------------------------------------------------- cpu baseline
 def cpu_baseline(seconds_budget: float):
     """The oracle (float64 NumPy, as it stands) on a bounded sample of the same workload: one
@@ -582,6 +618,8 @@ def main():
         out["sweep"] = sweep(af, w, shape)
         log("stress workload (8 pipelines, M = 2264, 32 layers)")
         out["stress"] = stress(af, w, shape)
+        log("K sweep (K = 7, 16, 24, 32)")
+        out["k_sweep"] = k_sweep(af, w, shape, pids)
     ring.close()
     w.close()
     torch.cuda.empty_cache()

@@ -75,6 +75,7 @@ struct AttnArgs {
   const DevSeg* segs;
   const int32_t* tiles;  // [n_tiles][2]: (segment, first row in segment); multi-row tiles first
   int n_multi;           // tiles of segments with more than one row (the rest are single rows)
+  int tile_base;         // set by the launcher: work tile of blockIdx.x = tile_base + blockIdx.x
   int n_heads, max_pos, ldq, ldo;  // row strides of q and o (>= H*hd)
   long ostride;              // > 0: o is written fragment-tiled (32-row blocks ostride apart)
   float scale_log2;          // log2(e) / sqrt(hd)
@@ -119,6 +120,7 @@ int gemm_splits(int dtype, int M, int N, int Kp);  // split-K factor that fills 
 int gemm_k_align();                  // K of the packed weights is a multiple of this
 
 constexpr int ATTN_BQ = 64;   // query rows per attention work tile
+constexpr int ATTN_WAVES = 8; // waves per attention workgroup (two key groups of four for query tiles)
 constexpr int ATTN_BKV = 64;  // keys per LDS tile
 constexpr int MAX_SEGMENTS = 4096;
 

@@ -848,8 +848,9 @@ __device__ __forceinline__ void attention_decode_row(const AttnArgs& a, int tile
   constexpr int KG = 64 / DG;       // value key groups (lane / DG)
   constexpr int KPL = 32 / KG;      // values: keys per lane per 32-key chunk
   static_assert(DG % 2 == 0 && DG <= 64 && 64 % DG == 0 && 32 % KG == 0, "head_dim");
-  __shared__ float wm[4], wl[4];
-  __shared__ __attribute__((aligned(16))) float wo[4][HD];
+  constexpr int NW = ATTN_WAVES;
+  __shared__ float wm[NW], wl[NW];
+  __shared__ __attribute__((aligned(16))) float wo[NW][HD];
   __shared__ __attribute__((aligned(16))) uint4 qs[DG];
   const int seg_i = a.tiles[2 * tile];
   const int h = blockIdx.y;
@@ -868,7 +869,7 @@ __device__ __forceinline__ void attention_decode_row(const AttnArgs& a, int tile
   float m_run = -INFINITY, l_run = 0.f, o[VEC];
 #pragma unroll
   for (int e = 0; e < VEC; ++e) o[e] = 0.f;
-  for (int c = wave; c * 32 < kv_len; c += 4) {
+  for (int c = wave; c * 32 < kv_len; c += NW) {
     // keys past kv_len read a clamped valid key and score -inf
     const int j = c * 32 + kl;
     const uint4* krow = (const uint4*)(Kg + (size_t)min(j, kv_len - 1) * HD) + half * KH2;
@@ -920,12 +921,14 @@ __device__ __forceinline__ void attention_decode_row(const AttnArgs& a, int tile
     for (int e = 0; e < VEC; ++e) wo[wave][dg * VEC + e] = o[e];
   __syncthreads();
   if (wave == 0 && lane < DG) {
-    const float M = fmaxf(fmaxf(wm[0], wm[1]), fmaxf(wm[2], wm[3]));
+    float M = wm[0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) M = fmaxf(M, wm[w]);
     float L = 0.f, acc[VEC];
 #pragma unroll
     for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
+    for (int w = 0; w < NW; ++w) {
       const float f = wm[w] == -INFINITY ? 0.f : exp2f(wm[w] - M);  // a wave with no chunk holds nothing
       L += wl[w] * f;
 #pragma unroll
@@ -955,10 +958,13 @@ __device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int ti
   static_assert((ATTN_BKV * CPR) % 256 == 0, "tile shape");
   typedef typename Mma<T>::frag frag;
 
-  __shared__ __attribute__((aligned(16))) T Ks[ATTN_BKV * KROW];
-  __shared__ __attribute__((aligned(16))) T Vt[HD * VROW];
+  // two key groups of four waves: group g takes key tiles g, g + 2, g + 4, .. of the segment
+  // with buffers of its own; the groups' partial softmax states are merged at the end
+  __shared__ __attribute__((aligned(16))) T Ks[2][ATTN_BKV * KROW];
+  __shared__ __attribute__((aligned(16))) T Vt[2][HD * VROW];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lane = threadIdx.x & 63, grp = threadIdx.x >> 8, wave = (threadIdx.x >> 6) & 3;
+  const int tid = threadIdx.x & 255;  // position within the key group
   const int lr = lane & 15, lg = lane >> 4;
   const int seg_i = a.tiles[2 * tile], i0 = a.tiles[2 * tile + 1];
   const int h = blockIdx.y;
@@ -1010,13 +1016,15 @@ __device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int ti
     }
   };
   const int n_kt = (kv_end + ATTN_BKV - 1) / ATTN_BKV;
-  load_tile(0);
-  for (int kt = 0; kt < n_kt; ++kt) {
+  const int n_it = (n_kt + 1) / 2;  // both groups run the same iterations (and barriers)
+  load_tile(grp * ATTN_BKV);        // keys past kv_end load as zeros
+  for (int it = 0; it < n_it; ++it) {
+    const int kt = 2 * it + grp;
     const int kb0 = kt * ATTN_BKV;
     // ---- park the tile in LDS: keys row-major, values transposed
     __syncthreads();  // the previous tile's LDS reads are done
 #pragma unroll
-    for (int j = 0; j < NCH; ++j) *(uint4*)(&Ks[(kr + KR * j) * KROW + kc * VEC]) = kreg[j];
+    for (int j = 0; j < NCH; ++j) *(uint4*)(&Ks[grp][(kr + KR * j) * KROW + kc * VEC]) = kreg[j];
     {
       T vt[NCH][VEC];
 #pragma unroll
@@ -1026,7 +1034,7 @@ __device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int ti
         T col[KPT];
 #pragma unroll
         for (int j = 0; j < KPT; ++j) col[j] = vt[j][e];
-        T* dst = &Vt[(vc * VEC + e) * VROW + vg * KPT];
+        T* dst = &Vt[grp][(vc * VEC + e) * VROW + vg * KPT];
         if constexpr (KPT * sizeof(T) == 4) {
           *(unsigned*)dst = *(const unsigned*)col;
         } else if constexpr (KPT * sizeof(T) == 8) {
@@ -1039,7 +1047,7 @@ __device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int ti
       }
     }
     __syncthreads();
-    if (kt + 1 < n_kt) load_tile(kb0 + ATTN_BKV);  // in flight while this tile is processed
+    if (kt + 2 < n_kt) load_tile(kb0 + 2 * ATTN_BKV);  // this group's next tile, in flight meanwhile
 
     if (wave_rows > 0 && kb0 <= wave_last_pos) {
       // ---- S^T = K . Q^T for 4 blocks of 16 keys
@@ -1050,7 +1058,7 @@ __device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int ti
         f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int s = 0; s < KST; ++s) {
-          const frag kf = *(const frag*)(&Ks[(kb * 16 + lr) * KROW + s * 32 + lg * 8]);
+          const frag kf = *(const frag*)(&Ks[grp][(kb * 16 + lr) * KROW + s * 32 + lg * 8]);
           sacc = Mma<T>::mma(kf, qf[s], sacc);
         }
 #pragma unroll
@@ -1064,13 +1072,17 @@ __device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int ti
       tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
       tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
       const float m_new = fmaxf(m_run, tmax);
-      const float corr = exp2f(m_run - m_new);  // m_run = -inf on the first tile -> 0
+      // a row may not have seen any key yet (key group 1's first tile can lie wholly past some
+      // rows): then every score so far is -inf, and 0 stands in as the reference so that the
+      // probabilities and the correction come out 0 instead of exp2(-inf - -inf)
+      const float m_ref = m_new == -INFINITY ? 0.f : m_new;
+      const float corr = exp2f(m_run - m_ref);  // m_run = -inf before the row's first key -> 0
       float psum = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float pe = exp2f(p[kb][e] - m_new);
+          const float pe = exp2f(p[kb][e] - m_ref);
           p[kb][e] = pe;
           psum += pe;
         }
@@ -1093,7 +1105,7 @@ __device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int ti
 #pragma unroll
         for (int d = 0; d < DB; ++d) {
           // keys lg * 4 .. +3 and 16 + lg * 4 .. +3 of the chunk: two aligned 4-element reads
-          const T* vrow = &Vt[(d * 16 + lr) * VROW + c * 32 + lg * 4];
+          const T* vrow = &Vt[grp][(d * 16 + lr) * VROW + c * 32 + lg * 4];
           frag vf;
           if constexpr (sizeof(T) == 2) {
             typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4_;
@@ -1118,6 +1130,31 @@ __device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int ti
     }
   }
 
+  // ---- merge key group 1 into group 0 (per lane: the same query and output dims in both)
+  constexpr int NF = 2 + 4 * DB;  // m, l, the output accumulators
+  static_assert(4 * 64 * NF * sizeof(float) <= sizeof(Ks), "merge buffer");
+  float* mb = (float*)&Ks[0][0] + (size_t)wave * NF * 64 + lane;
+  __syncthreads();  // every wave is done with the key/value buffers
+  if (grp == 1) {
+    mb[0] = m_run;
+    mb[64] = l_run;
+#pragma unroll
+    for (int d = 0; d < DB; ++d)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) mb[(2 + 4 * d + e) * 64] = oacc[d][e];
+  }
+  __syncthreads();
+  if (grp == 1) return;
+  {
+    const float m1 = mb[0], l1 = mb[64];
+    const float M = fmaxf(m_run, m1);
+    const float f0 = m_run == -INFINITY ? 0.f : exp2f(m_run - M), f1 = m1 == -INFINITY ? 0.f : exp2f(m1 - M);
+    l_run = l_run * f0 + l1 * f1;
+#pragma unroll
+    for (int d = 0; d < DB; ++d)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) oacc[d][e] = oacc[d][e] * f0 + mb[(2 + 4 * d + e) * 64] * f1;
+  }
   if (wave_rows <= 0 || !q_ok) return;
   float l_tot = l_run + __shfl_xor(l_run, 16);
   l_tot += __shfl_xor(l_tot, 32);
@@ -1142,22 +1179,35 @@ __device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int ti
 // One launch for the whole step: work tiles [0, n_multi) are query tiles of multi-row segments
 // (ordered longest first, so they start first), the rest single-row segments.
 template <typename T, int HD, bool PREFILL>
-__global__ __launch_bounds__(256, !PREFILL ? 4 : (sizeof(T) == 4 && HD == 128) ? 1 : 3) void attention_kernel(AttnArgs a) {
+__global__ __launch_bounds__(64 * ATTN_WAVES, !PREFILL ? 4 : 2) void attention_kernel(AttnArgs a) {
+  const int tile = a.tile_base + blockIdx.x;
   if constexpr (PREFILL) {
-    if ((int)blockIdx.x < a.n_multi) {
-      attention_prefill_tile<T, HD>(a, blockIdx.x);
+    if (tile < a.n_multi) {
+      attention_prefill_tile<T, HD>(a, tile);
       return;
     }
   }
-  attention_decode_row<T, HD>(a, blockIdx.x);
+  attention_decode_row<T, HD>(a, tile);
 }
 
+// Query tiles and decode rows share one launch, query tiles first; the decode-only kernel has
+// no query-tile LDS and registers and so fits more workgroups per CU, which pays once the decode
+// rows alone would more than fill the GPU twice over (a second launch then costs less).
 template <typename T, int HD>
-static void attention_launch(const AttnArgs& a, int n_tiles, hipStream_t s) {
-  if (a.n_multi > 0)
-    hipLaunchKernelGGL((attention_kernel<T, HD, true>), dim3(n_tiles, a.n_heads), dim3(256), 0, s, a);
-  else  // decode rows only: without the prefill path's LDS and registers
-    hipLaunchKernelGGL((attention_kernel<T, HD, false>), dim3(n_tiles, a.n_heads), dim3(256), 0, s, a);
+static void attention_launch(const AttnArgs& a0, int n_tiles, hipStream_t s) {
+  AttnArgs a = a0;
+  a.tile_base = 0;
+  const dim3 block(64 * ATTN_WAVES);
+  const int n_single = n_tiles - a.n_multi;
+  if (a.n_multi == 0) {
+    hipLaunchKernelGGL((attention_kernel<T, HD, false>), dim3(n_tiles, a.n_heads), block, 0, s, a);
+  } else if ((long)n_single * a.n_heads <= 512) {
+    hipLaunchKernelGGL((attention_kernel<T, HD, true>), dim3(n_tiles, a.n_heads), block, 0, s, a);
+  } else {
+    hipLaunchKernelGGL((attention_kernel<T, HD, true>), dim3(a.n_multi, a.n_heads), block, 0, s, a);
+    a.tile_base = a.n_multi;
+    hipLaunchKernelGGL((attention_kernel<T, HD, false>), dim3(n_single, a.n_heads), block, 0, s, a);
+  }
 }
 
 // tiles[0, n_multi) are query tiles of multi-row segments, tiles[n_multi, n_tiles) the

@@ -44,7 +44,8 @@ def allclose_report(got, ref, atol, rtol):
     ref = np.asarray(ref, dtype=np.float64)
     err = np.abs(got - ref)
     bound = atol + rtol * np.abs(ref)
-    bad = err > bound
+    bad = ~(err <= bound)  # a NaN or infinite result counts as bad
+    err = np.where(np.isfinite(err), err, np.inf)
     return dict(ok=not bad.any(), n_bad=int(bad.sum()), max_abs=float(err.max(initial=0.0)),
                 max_rel=float((err / np.maximum(np.abs(ref), 1e-30)).max(initial=0.0)),
                 rms=float(np.sqrt(np.mean(err ** 2))) if err.size else 0.0)
