@@ -433,6 +433,52 @@ def k_sweep(af, w, shape, pids, Ks=(7, 16, 24, 32), steps=12):
     return out
 
 
+def copy_shift(af, w, shape, pids, pool, K=7, steps=12, reps=10):
+    """The paper's physical-copy InPlaceKVShift against the index rotation: the same pipeline
+    (K = 7) with stage s kept in slot s and every live stage's keys and values copied one slot
+    along after each step (af_ring_shift_stages); and that copy alone, on a steady-state ring
+    (stages of 276 .. 281 positions, all 32 layers), with the bytes it moves."""
+    import torch
+    from paper_2512_20276_amd.pipeline import Pipeline
+    L_P = int(pids.numel())
+    ring = af.Ring(shape.n_layers, K, 288, shape.n_heads, shape.head_dim, dtype=torch.bfloat16)
+    pipe = Pipeline(w, ring, K, pids, lambda t: pool[t % len(pool)], keep_history=False, shift="copy")
+    for _ in range(K + 1):
+        pipe.step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        pipe.step()
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / steps
+    ring.close()
+    # the copy alone: K - 1 live stages of L_P .. L_P + K - 2 positions
+    ring = af.Ring(shape.n_layers, K, 288, shape.n_heads, shape.head_dim, dtype=torch.bfloat16)
+    lens = [L_P + s for s in range(K - 1)]
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    total_ms = 0.0
+    for r in range(reps + 1):
+        ring.reset()
+        for s, n in enumerate(lens):
+            ring.append(s, n)
+        ring.append(10 ** 6, 1)   # the last stage's slot, released: the finished request
+        ring.release(10 ** 6)
+        torch.cuda.synchronize()
+        e0.record()
+        ring.shift_stages(K)
+        e1.record()
+        torch.cuda.synchronize()
+        if r:
+            total_ms += e0.elapsed_time(e1)
+    ring.close()
+    shift_ms = total_ms / reps
+    moved = 2 * sum(lens) * shape.n_heads * shape.head_dim * 2 * 2 * shape.n_layers  # read + write
+    return {"ms_per_step": round(dt * 1e3, 3), "packed_steps_per_s": round(1 / dt, 3),
+            "shift_ms_per_step": round(shift_ms, 4), "shift_bytes_per_step": moved,
+            "shift_GB/s": round(moved / (shift_ms * 1e-3) / 1e9, 1),
+            "note": "stage s kept in slot s; K - 1 stages' keys and values copied one slot along per step"}
+
+
 # ----------------------------------------------------------------------------- cpu baseline
 def cpu_baseline(seconds_budget: float):
     """The oracle (float64 NumPy, as it stands) on a bounded sample of the same workload: one
@@ -620,6 +666,8 @@ def main():
         out["stress"] = stress(af, w, shape)
         log("K sweep (K = 7, 16, 24, 32)")
         out["k_sweep"] = k_sweep(af, w, shape, pids)
+        log("physical-copy stage shift (the paper's InPlaceKVShift copy) against the rotation")
+        out["copy_shift"] = copy_shift(af, w, shape, pids, pool, K)
     ring.close()
     w.close()
     torch.cuda.empty_cache()

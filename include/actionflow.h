@@ -106,6 +106,19 @@ af_status af_ring_append(af_ring* ring, int64_t request_id, int32_t n_new, af_se
  * AF_ERR_UNKNOWN_REQUEST if the id owns no slot. */
 af_status af_ring_release(af_ring* ring, int64_t request_id);
 
+/* InPlaceKVShift as the paper's physical copy (Alg. 2, Sec. 3.3): the stage regions move
+ * one stage along, so that stage s's request ends up in slot s + 1.  For s = n_stages - 2
+ * down to 0, the request in slot s (if any) is moved to slot s + 1: its keys and values
+ * (every layer, positions 0 .. len - 1) are copied on hip_stream and its bookkeeping moves
+ * with it; slot 0 is left free and the rotation head is set to 0, so the next new request
+ * takes slot 0.  Slot n_stages - 1 must be free when the call is made (the finished request
+ * released; AF_ERR_SLOT_BUSY otherwise); slots >= n_stages are untouched.
+ * 2 <= n_stages <= n_slots, else AF_ERR_INVALID_ARG.  The attention inputs are the same as
+ * with the index rotation of af_ring_append; this is the variant that moves bytes.
+ * A bookkeeping-only ring (n_layers = 0) moves only the bookkeeping.  A failed call
+ * changes nothing. */
+af_status af_ring_shift_stages(af_ring* ring, int32_t n_stages, void* hip_stream);
+
 /* Copies the bookkeeping to host arrays: owners[n_slots] (request id, -1 = free),
  * lens[n_slots], *head (next slot a new request takes).  Any pointer may be NULL. */
 af_status af_ring_state(const af_ring* ring, int64_t* owners, int32_t* lens, int32_t* head);

@@ -73,6 +73,23 @@ class RingModel:
         self.length[slot] = 0
         return slot
 
+    def shift_stages(self, n_stages: int) -> None:
+        """The paper's physical InPlaceKVShift: the request of slot s moves to slot s + 1 for
+        s = n_stages - 2 .. 0 (slot n_stages - 1 must be free), slot 0 is left free and the
+        next new request takes it."""
+        if n_stages < 2 or n_stages > self.n_slots:
+            raise RingError(INVALID_ARG, "n_stages outside [2, n_slots]")
+        if self.owner[n_stages - 1] != self.FREE:
+            raise RingError(SLOT_BUSY, f"slot {n_stages - 1} still owned")
+        for s in range(n_stages - 2, -1, -1):
+            rid = self.owner[s]
+            if rid == self.FREE:
+                continue
+            self.owner[s + 1], self.length[s + 1] = rid, self.length[s]
+            self._slot_of[rid] = s + 1
+            self.owner[s], self.length[s] = self.FREE, 0
+        self.head = 0
+
     def slot_of(self, request_id: int) -> Optional[int]:
         return self._slot_of.get(request_id)
 

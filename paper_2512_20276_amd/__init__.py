@@ -72,6 +72,7 @@ def _load():
         "af_ring_append": (I32, [P, I64, I32, SEG]),
         "af_ring_release": (I32, [P, I64]),
         "af_ring_state": (I32, [P, C.POINTER(I64), C.POINTER(I32), C.POINTER(I32)]),
+        "af_ring_shift_stages": (I32, [P, I32, P]),
         "af_ring_write_kv": (I32, [P, I32, I32, I32, I32, P, P, P]),
         "af_ring_read_kv": (I32, [P, I32, I32, I32, I32, P, P, P]),
         "af_weights_tensor_count": (I32, [I32]),
@@ -184,6 +185,10 @@ class Ring:
 
     def release(self, request_id: int):
         _check(lib.af_ring_release(self.h, request_id))
+
+    def shift_stages(self, n_stages: int, stream=None):
+        """InPlaceKVShift by physical copy: slot s -> s + 1 for s < n_stages - 1 (see the header)."""
+        _check(lib.af_ring_shift_stages(self.h, n_stages, _stream(stream) if self.desc.n_layers > 0 else None))
 
     def state(self):
         n = self.desc.n_slots

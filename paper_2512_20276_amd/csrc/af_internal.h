@@ -98,6 +98,11 @@ hipError_t launch_to_frag(int dtype, const void* x, int ld, int M, int K, int Kp
 hipError_t launch_embed(int dtype, const int32_t* ids, const void* table, int vocab, const void* embeds, void* out,
                         int M, int D, int32_t* err_count, hipStream_t s);
 hipError_t launch_argmax(const float* logits, int n_rows, int V, int32_t* tokens, hipStream_t s);
+// Copies n_runs runs of run_bytes (16-byte multiple, 16-byte aligned): run r goes from
+// base + src + (r / per_group) * group_stride + (r % per_group) * run_stride to the same
+// place with dst in place of src (byte offsets).
+hipError_t launch_run_copy(void* base, size_t src, size_t dst, int n_runs, int per_group, size_t group_stride,
+                           size_t run_stride, size_t run_bytes, hipStream_t s);
 // Fragment-tiles N rows of K elements (padded to Kp, a multiple of 32) for the GEMM; srcs is a
 // device array of source pointers, map (device, optional) gives (source, row) per output row.
 hipError_t launch_frag_pack(int dtype, void* dst, long bstride, const void* const* srcs, const int32_t* map, int N,

@@ -1477,6 +1477,27 @@ hipError_t launch_argmax(const float* logits, int n_rows, int V, int32_t* tokens
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ ring stage move
+// One workgroup per run, 16-byte copies.
+__global__ __launch_bounds__(256) void run_copy_kernel(char* base, size_t src, size_t dst, int per_group,
+                                                       size_t group_stride, size_t run_stride, size_t run_bytes) {
+  const int r = blockIdx.x;
+  const size_t off = (size_t)(r / per_group) * group_stride + (size_t)(r % per_group) * run_stride;
+  const uint4* from = (const uint4*)(base + src + off);
+  uint4* to = (uint4*)(base + dst + off);
+  for (size_t i = threadIdx.x; i < run_bytes / 16; i += 256) to[i] = from[i];
+}
+
+hipError_t launch_run_copy(void* base, size_t src, size_t dst, int n_runs, int per_group, size_t group_stride,
+                           size_t run_stride, size_t run_bytes, hipStream_t s) {
+  if (n_runs <= 0 || run_bytes == 0) return hipSuccess;
+  if (run_bytes % 16 || src % 16 || dst % 16 || group_stride % 16 || run_stride % 16 || per_group <= 0)
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(run_copy_kernel, dim3(n_runs), dim3(256), 0, s, (char*)base, src, dst, per_group, group_stride,
+                     run_stride, run_bytes);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ weight repacking
 // dst: fragment-tiled [N/16][Kp/32][64 lanes][8] (see the GEMM); source row n is
 // srcs[map[2n]] row map[2n+1] (or src0 row n without a map), rows of K elements, k >= K zero.

@@ -174,6 +174,49 @@ extern "C" af_status af_ring_release(af_ring* ring, int64_t request_id) {
   return AF_OK;
 }
 
+extern "C" af_status af_ring_shift_stages(af_ring* ring, int32_t n_stages, void* hip_stream) {
+  clear_error();
+  if (!ring) {
+    set_error("af_ring_shift_stages: NULL ring");
+    return AF_ERR_INVALID_ARG;
+  }
+  if (n_stages < 2 || n_stages > ring->d.n_slots) {
+    set_error("af_ring_shift_stages: n_stages %d outside [2, %d]", n_stages, ring->d.n_slots);
+    return AF_ERR_INVALID_ARG;
+  }
+  if (ring->owner[n_stages - 1] != -1) {
+    set_error("af_ring_shift_stages: slot %d (the last stage) still holds request %lld", n_stages - 1,
+              (long long)ring->owner[n_stages - 1]);
+    return AF_ERR_SLOT_BUSY;
+  }
+  const hipStream_t s = (hipStream_t)hip_stream;
+  const size_t es = dtype_size(ring->d.dtype);
+  const int H = ring->d.n_kv_heads, hd = ring->d.head_dim;
+  for (int st = n_stages - 2; st >= 0; --st) {
+    const int64_t rid = ring->owner[st];
+    if (rid == -1) continue;
+    const int n = ring->len[st];
+    if (ring->kv && n > 0) {
+      // runs: (layer, k|v) groups of H heads, each head's positions 0 .. n - 1 contiguous
+      const size_t src = ring->offset(0, 0, st, 0, 0) * es, dst = ring->offset(0, 0, st + 1, 0, 0) * es;
+      const size_t group = ring->kv_region() * es, head = (size_t)ring->d.max_pos * hd * es;
+      hipError_t e = launch_run_copy(ring->kv, src, dst, 2 * ring->d.n_layers * H, H, group, head,
+                                     (size_t)n * hd * es, s);
+      if (e != hipSuccess) {
+        set_error("af_ring_shift_stages: copy of slot %d failed: %s", st, hipGetErrorString(e));
+        return AF_ERR_DEVICE;
+      }
+    }
+    ring->owner[st + 1] = rid;
+    ring->len[st + 1] = n;
+    ring->slot_of[rid] = st + 1;
+    ring->owner[st] = -1;
+    ring->len[st] = 0;
+  }
+  ring->head = 0;
+  return AF_OK;
+}
+
 extern "C" af_status af_ring_state(const af_ring* ring, int64_t* owners, int32_t* lens, int32_t* head) {
   clear_error();
   if (!ring) {

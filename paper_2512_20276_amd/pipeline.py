@@ -9,6 +9,11 @@ Several independent pipelines (``n_pipes`` = P) can share one forward: step t th
 the P prefills first and then stage 1 of every pipeline, stage 2 of every pipeline, and so
 on (Eq. (1) with each stage widened to P rows).  Request ids are t * P + p.
 
+With ``shift="copy"`` (one pipeline) the stage regions move instead, as the paper's
+InPlaceKVShift copy does: stage s always sits in slot s, and after each step the ring
+copies every live request's keys and values one slot along (af_ring_shift_stages).  The
+attention inputs, and so every output, are the same as with the rotation; only bytes move.
+
 Token feedback stays on the device: the step's greedy tokens are written by the library
 straight into the next step's id buffer.  Stage s of step t feeds stage s+1 of step t+1,
 and in this row order the stages' tokens (segment order: stage-major) are exactly the next
@@ -47,9 +52,12 @@ class Pipeline:
 
     def __init__(self, weights: Weights, ring: Ring, K: int, prefill_ids: torch.Tensor,
                  prefill_embeds: Callable[[int], torch.Tensor], keep_logits: bool = False,
-                 keep_history: bool = True, stream=None, n_pipes: int = 1):
+                 keep_history: bool = True, stream=None, n_pipes: int = 1, shift: str = "rotate"):
         if K < 1 or n_pipes < 1:
             raise ValueError("K >= 1 and n_pipes >= 1")
+        if shift not in ("rotate", "copy") or (shift == "copy" and (n_pipes != 1 or K < 2)):
+            raise ValueError("shift is 'rotate', or 'copy' for one pipeline with K >= 2")
+        self.shift = shift
         self.w, self.ring, self.K, self.P = weights, ring, K, n_pipes
         self.L_P = int(prefill_ids.numel())
         self.prefill_embeds = prefill_embeds
@@ -100,6 +108,8 @@ class Pipeline:
                 self.counts[s.request_id] = c
         for rid in done:
             self.ring.release(rid)
+        if self.shift == "copy":
+            self.ring.shift_stages(self.K, self.stream)
         return done
 
     def step(self) -> StepResult:

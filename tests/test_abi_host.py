@@ -173,3 +173,51 @@ def test_multi_pipeline_bookkeeping_matches_oracle_and_closed_form(P, K, n_slots
             model.release(rid)
         assert ring.state() == model.state()
     ring.close()
+
+
+@pytest.mark.parametrize("K,n_slots", [(7, 7), (7, 9), (3, 3), (2, 4)])
+def test_copy_shift_bookkeeping_matches_oracle(K, n_slots):
+    """The physical-copy InPlaceKVShift on a bookkeeping-only ring: the driver's copy mode gives
+    the same segment tables and slot state as the oracle RingModel, and stage s of every step
+    sits in slot s (closed form), with pos0 = L_P + s - 1."""
+    import types
+
+    import torch
+
+    from paper_2512_20276_amd.pipeline import Pipeline
+
+    L_P = 20
+    ring = af.Ring(0, n_slots, 64)
+    model = RingModel(n_slots, 64)
+    w = types.SimpleNamespace(shape=types.SimpleNamespace(d_model=8, vocab=4), dtype=torch.float32)
+    pipe = Pipeline(w, ring, K, torch.full((L_P,), -1, dtype=torch.int32), lambda t: None, shift="copy")
+    for t in range(3 * K + 1):
+        segs, _ = pipe.reserve(t)
+        for s, sg in enumerate(segs):
+            assert (sg.slot, sg.pos0) == model.append(t - s, L_P if s == 0 else 1)
+            assert sg.slot == s and sg.pos0 == (0 if s == 0 else L_P + s - 1)
+        done = pipe.finish(segs)
+        for rid in done:
+            model.release(rid)
+        model.shift_stages(K)
+        assert ring.state() == model.state()
+
+
+def test_copy_shift_errors_leave_state_unchanged():
+    ring = af.Ring(0, 4, 16)
+    model = RingModel(4, 16)
+    for rid in range(3):
+        ring.append(rid, 2)
+        model.append(rid, 2)
+    before = ring.state()
+    for n, code in ((1, af.AF_ERR_INVALID_ARG), (5, af.AF_ERR_INVALID_ARG), (3, af.AF_ERR_SLOT_BUSY)):
+        with pytest.raises(af.AFError) as e:
+            ring.shift_stages(n)
+        assert e.value.code == code
+        with pytest.raises(RingError) as e2:
+            model.shift_stages(n)
+        assert e2.value.code == code
+        assert ring.state() == before == model.state()
+    ring.shift_stages(4)
+    model.shift_stages(4)
+    assert ring.state() == model.state() == ([-1, 0, 1, 2], [0, 2, 2, 2], 0)

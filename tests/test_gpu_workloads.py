@@ -165,3 +165,74 @@ def test_stress_pipelines_pack_independently_32_layers():
         assert len(toks[(0, p)]) == K
         sring.close()
     w.close()
+
+
+# ----------------------------------------------------------------------------- physical-copy shift
+def test_shift_stages_moves_ring_contents():
+    """af_ring_shift_stages copies each live stage's keys and values (every layer, positions
+    0 .. len - 1) one slot along, bit for bit, and leaves slots past the stages untouched."""
+    H, hd, L, n_slots, max_pos, K = 4, 64, 3, 6, 40, 4
+    ring = af.Ring(L, n_slots, max_pos, H, hd, dtype=torch.bfloat16)
+    lens = {0: 9, 1: 21, 2: 33}                 # stages 0..2 live, slot 3 (the last stage) free
+    for slot, n in lens.items():
+        ring.append(100 + slot, n)
+    ring.append(999, 5)                         # slot 3, then released: the finished request
+    ring.release(999)
+    before = {}
+    for l in range(L):
+        for slot in range(n_slots):
+            kv = wl.draw(("shift", l, slot), (2, max_pos, H, hd), device="cuda")
+            ring.write_kv(l, slot, 0, kv[0], kv[1])
+            before[(l, slot)] = (to_np(kv[0]), to_np(kv[1]))
+    ring.shift_stages(K)
+    torch.cuda.synchronize()
+    owners, lengths, head = ring.state()
+    assert owners[:4] == [-1, 100, 101, 102] and lengths[:4] == [0, 9, 21, 33] and head == 0
+    for l in range(L):
+        for slot, n in lens.items():
+            k, v = ring.read_kv(l, slot + 1, 0, n)
+            assert np.array_equal(to_np(k), before[(l, slot)][0][:n]), (l, slot)
+            assert np.array_equal(to_np(v), before[(l, slot)][1][:n]), (l, slot)
+        for slot in (4, 5):
+            k, v = ring.read_kv(l, slot, 0, max_pos)
+            assert np.array_equal(to_np(k), before[(l, slot)][0]) and np.array_equal(to_np(v), before[(l, slot)][1])
+    ring.close()
+
+
+@pytest.mark.timeout(600)
+def test_copy_shift_pipeline_equals_rotation_32_layers():
+    """The paper's physical-copy InPlaceKVShift and this build's index rotation give attention
+    the same keys and values, so the whole 32-layer pipeline produces identical rows, logits
+    and tokens (K = 7, through the first full step and beyond)."""
+    shape = wl.LLAMA7B
+    K, L_V, L_T = 7, 256, 20
+    L_P, D = L_V + L_T, shape.d_model
+    g, layers = wl.model_weights(shape, seed=0, device="cuda")
+    w = af.Weights(shape, g, layers)
+    del g, layers
+    text = wl.draw_ids(("instruction", 0), L_T, shape.vocab, device="cuda")
+    pids = torch.cat([torch.full((L_V,), -1, dtype=torch.int32, device="cuda"), text])
+    pool = {}
+
+    def embeds(t):
+        if t not in pool:
+            e = torch.zeros((L_P + K - 1, D), dtype=torch.bfloat16, device="cuda")
+            e[:L_V] = wl.draw(("vision", 0, t), (L_V, D), device="cuda")
+            pool[t] = e
+        return pool[t]
+
+    out = {}
+    for mode, n_slots in (("rotate", 8), ("copy", 7)):
+        ring = af.Ring(shape.n_layers, n_slots, 288, shape.n_heads, shape.head_dim, dtype=torch.bfloat16)
+        pipe = Pipeline(w, ring, K, pids, embeds, keep_logits=True, shift=mode)
+        rows = []
+        for t in range(K + 2):
+            res = pipe.step()
+            rows.append((to_np(res.hidden), to_np(res.logits), res.tokens.cpu().tolist()))
+            if mode == "copy":
+                assert [sg[2] for sg in res.segments] == list(range(len(res.segments)))
+        out[mode] = rows
+        ring.close()
+    for t, (a, b) in enumerate(zip(out["rotate"], out["copy"])):
+        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]) and a[2] == b[2], t
+    w.close()
