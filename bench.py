@@ -479,6 +479,35 @@ def copy_shift(af, w, shape, pids, pool, K=7, steps=12, reps=10):
             "note": "stage s kept in slot s; K - 1 stages' keys and values copied one slot along per step"}
 
 
+def naive_pipe(af, w, shape, pids, pool, packed_ms, K=7, steps=12):
+    """The pipeline without the unified ring (the paper's Naive Pipe ablation): per-request
+    caches, every layer's histories gathered into one contiguous buffer and the new rows
+    scattered back, the host waiting for the device after each layer and building the next
+    batch from host-side tokens; and the same with the per-layer waits left out (the copies'
+    cost alone).  Wall-clock ms per steady-state step (K = 7, M = 282)."""
+    import torch
+    from paper_2512_20276_amd.naive_pipe import NaivePipeline
+    out = {}
+    for name, sync in (("host_sync_per_layer", True), ("copies_only", False)):
+        pipe = NaivePipeline(w, K, pids, lambda t: pool[t % len(pool)], sync_per_layer=sync)
+        for _ in range(K + 1):
+            pipe.step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            pipe.step()
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / steps
+        out[name] = {"ms_per_step": round(dt * 1e3, 3), "packed_steps_per_s": round(1 / dt, 3),
+                     "ring_speedup": round(dt * 1e3 / packed_ms, 3)}
+        out["copy_bytes_per_step"] = pipe.copy_bytes
+        pipe.close()
+    out["note"] = ("per layer: K - 1 histories gathered and K new rows scattered back (copy_bytes: bytes "
+                   "copied, each read once and written once); ring_speedup = this ms per step / the ring "
+                   "pipeline's")
+    return out
+
+
 # ----------------------------------------------------------------------------- cpu baseline
 def cpu_baseline(seconds_budget: float):
     """The oracle (float64 NumPy, as it stands) on a bounded sample of the same workload: one
@@ -668,6 +697,8 @@ def main():
         out["k_sweep"] = k_sweep(af, w, shape, pids)
         log("physical-copy stage shift (the paper's InPlaceKVShift copy) against the rotation")
         out["copy_shift"] = copy_shift(af, w, shape, pids, pool, K)
+        log("naive pipe (per-request caches, per-layer gather/scatter, host-coordinated)")
+        out["naive_pipe"] = naive_pipe(af, w, shape, pids, pool, ms_step, K)
     ring.close()
     w.close()
     torch.cuda.empty_cache()

@@ -133,6 +133,16 @@ af_status af_ring_write_kv(af_ring* ring, int32_t layer, int32_t slot, int32_t p
 af_status af_ring_read_kv(af_ring* ring, int32_t layer, int32_t slot, int32_t pos0, int32_t n,
                           void* k, void* v, void* hip_stream);
 
+/* Copies keys and values of positions [pos0, pos0 + n), all heads, from (src_layer, src_slot)
+ * of ring src to (dst_layer, dst_slot) of ring dst, one kernel on hip_stream.  The rings must
+ * agree in n_kv_heads, head_dim and dtype and hold the region (else AF_ERR_INVALID_ARG or
+ * AF_ERR_OUT_OF_RANGE, nothing launched); a region onto itself is a no-op.  Bookkeeping is
+ * not touched.  This is the per-request gather into a contiguous buffer (and the scatter
+ * back) that a pipeline without the unified ring needs before every layer's attention
+ * (Sec. 3.1, Sec. 3.3); the ring's own forward never calls it. */
+af_status af_ring_copy_kv(const af_ring* src, int32_t src_layer, int32_t src_slot, af_ring* dst,
+                          int32_t dst_layer, int32_t dst_slot, int32_t pos0, int32_t n, void* hip_stream);
+
 /* ------------------------------------------------------------------ weights */
 
 /* Number of tensors af_weights_create expects for n_layers layers: 3 + 9 * n_layers. */
@@ -173,6 +183,14 @@ af_status af_packed_forward(af_weights* w, const int32_t* token_ids, const void*
  * rules as af_packed_forward.  Used for per-layer parity and single-layer timing. */
 af_status af_packed_layer_forward(af_weights* w, int32_t layer, void* hidden_inout, int32_t M,
                                   const af_segment* segs, int32_t n_seg, af_ring* ring, void* hip_stream);
+
+/* The same with the layer's keys and values in ring layer ring_layer (layer `layer` of the
+ * weights): for a ring that holds one layer at a time, as the per-layer gather buffer of a
+ * pipeline without the unified ring does.  ring_layer < 0 or >= the ring's layers is
+ * AF_ERR_OUT_OF_RANGE / AF_ERR_INVALID_ARG. */
+af_status af_packed_layer_forward_kv(af_weights* w, int32_t layer, void* hidden_inout, int32_t M,
+                                     const af_segment* segs, int32_t n_seg, af_ring* ring, int32_t ring_layer,
+                                     void* hip_stream);
 
 /* Options of the forward (bit flags; default 0):
  *  AF_OPT_NO_SPLIT_K  never split a projection's K range over workgroups.  Every kernel then

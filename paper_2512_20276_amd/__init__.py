@@ -75,11 +75,13 @@ def _load():
         "af_ring_shift_stages": (I32, [P, I32, P]),
         "af_ring_write_kv": (I32, [P, I32, I32, I32, I32, P, P, P]),
         "af_ring_read_kv": (I32, [P, I32, I32, I32, I32, P, P, P]),
+        "af_ring_copy_kv": (I32, [P, I32, I32, P, I32, I32, I32, I32, P]),
         "af_weights_tensor_count": (I32, [I32]),
         "af_weights_create": (I32, [C.POINTER(ModelDesc), PP, I32, P, PP]),
         "af_weights_destroy": (I32, [P]),
         "af_packed_forward": (I32, [P, P, P, I32, SEG, I32, P, P, P, P, P]),
         "af_packed_layer_forward": (I32, [P, I32, P, I32, SEG, I32, P, P]),
+        "af_packed_layer_forward_kv": (I32, [P, I32, P, I32, SEG, I32, P, I32, P]),
         "af_weights_device_errors": (I32, [P, P, C.POINTER(I32)]),
         "af_op_embed": (I32, [P, P, P, I32, P, P]),
         "af_op_rmsnorm": (I32, [I32, P, P, P, I32, I32, F32, P]),
@@ -199,6 +201,10 @@ class Ring:
     def write_kv(self, layer, slot, pos0, k: torch.Tensor, v: torch.Tensor, stream=None):
         _check(lib.af_ring_write_kv(self.h, layer, slot, pos0, k.shape[0], _ptr(k), _ptr(v), _stream(stream)))
 
+    def copy_kv_to(self, layer, slot, dst: "Ring", dst_layer, dst_slot, pos0, n, stream=None):
+        """Keys and values of positions [pos0, pos0 + n) of (layer, slot) into dst's (dst_layer, dst_slot)."""
+        _check(lib.af_ring_copy_kv(self.h, layer, slot, dst.h, dst_layer, dst_slot, pos0, n, _stream(stream)))
+
     def read_kv(self, layer, slot, pos0, n, stream=None):
         d = self.desc
         k = torch.empty((n, d.n_kv_heads, d.head_dim), dtype=self.dtype, device="cuda")
@@ -268,10 +274,16 @@ def packed_forward(w: Weights, token_ids: torch.Tensor, embeds: Optional[torch.T
                                  _ptr(out_hidden), _ptr(out_logits), _ptr(out_tokens), _stream(stream)))
 
 
-def packed_layer_forward(w: Weights, layer: int, hidden: torch.Tensor, segs, ring: Ring, stream=None):
+def packed_layer_forward(w: Weights, layer: int, hidden: torch.Tensor, segs, ring: Ring, stream=None,
+                         ring_layer: Optional[int] = None):
+    """One layer in place on hidden; its keys and values in ring layer ``ring_layer`` (default ``layer``)."""
     sa = segs if isinstance(segs, C.Array) else segments_array(segs)
-    _check(lib.af_packed_layer_forward(w.h, layer, _ptr(hidden), hidden.shape[0], sa, len(sa), ring.h,
-                                       _stream(stream)))
+    if ring_layer is None:
+        _check(lib.af_packed_layer_forward(w.h, layer, _ptr(hidden), hidden.shape[0], sa, len(sa), ring.h,
+                                           _stream(stream)))
+    else:
+        _check(lib.af_packed_layer_forward_kv(w.h, layer, _ptr(hidden), hidden.shape[0], sa, len(sa), ring.h,
+                                              ring_layer, _stream(stream)))
 
 
 def op_embed(w: Weights, token_ids, embeds, out, stream=None):

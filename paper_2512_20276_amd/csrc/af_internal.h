@@ -98,9 +98,15 @@ hipError_t launch_to_frag(int dtype, const void* x, int ld, int M, int K, int Kp
 hipError_t launch_embed(int dtype, const int32_t* ids, const void* table, int vocab, const void* embeds, void* out,
                         int M, int D, int32_t* err_count, hipStream_t s);
 hipError_t launch_argmax(const float* logits, int n_rows, int V, int32_t* tokens, hipStream_t s);
-// Copies n_runs runs of run_bytes (16-byte multiple, 16-byte aligned): run r goes from
-// base + src + (r / per_group) * group_stride + (r % per_group) * run_stride to the same
-// place with dst in place of src (byte offsets).
+// Byte strides of a run copy: run r starts at (r / per_group) * group + (r % per_group) * run.
+struct CopyStrides {
+  size_t src_group, src_run, dst_group, dst_run;
+};
+// Copies n_runs runs of run_bytes (16-byte multiple, 16-byte aligned) from src to dst at the
+// run offsets of st.  Runs must not overlap one another.
+hipError_t launch_copy_runs(const void* src, void* dst, int n_runs, int per_group, const CopyStrides& st,
+                            size_t run_bytes, hipStream_t s);
+// The same within one buffer: from base + src to base + dst (byte offsets), equal strides.
 hipError_t launch_run_copy(void* base, size_t src, size_t dst, int n_runs, int per_group, size_t group_stride,
                            size_t run_stride, size_t run_bytes, hipStream_t s);
 // Fragment-tiles N rows of K elements (padded to Kp, a multiple of 32) for the GEMM; srcs is a

@@ -1477,25 +1477,36 @@ hipError_t launch_argmax(const float* logits, int n_rows, int V, int32_t* tokens
   return hipGetLastError();
 }
 
-// ------------------------------------------------------------------ ring stage move
-// One workgroup per run, 16-byte copies.
-__global__ __launch_bounds__(256) void run_copy_kernel(char* base, size_t src, size_t dst, int per_group,
-                                                       size_t group_stride, size_t run_stride, size_t run_bytes) {
+// ------------------------------------------------------------------ ring region copies
+// Stage moves and copies between rings: 16-byte copies, one workgroup per 64 KiB of a run.
+__global__ __launch_bounds__(256) void run_copy_kernel(const char* src, char* dst, int per_group, CopyStrides st,
+                                                       size_t run_bytes) {
   const int r = blockIdx.x;
-  const size_t off = (size_t)(r / per_group) * group_stride + (size_t)(r % per_group) * run_stride;
-  const uint4* from = (const uint4*)(base + src + off);
-  uint4* to = (uint4*)(base + dst + off);
-  for (size_t i = threadIdx.x; i < run_bytes / 16; i += 256) to[i] = from[i];
+  const size_t g = (size_t)(r / per_group), h = (size_t)(r % per_group);
+  const uint4* from = (const uint4*)(src + g * st.src_group + h * st.src_run);
+  uint4* to = (uint4*)(dst + g * st.dst_group + h * st.dst_run);
+  const size_t n16 = run_bytes / 16, chunk = (size_t)blockIdx.y * 4096;  // 64 KiB per block
+  const size_t end = n16 < chunk + 4096 ? n16 : chunk + 4096;
+  for (size_t i = chunk + threadIdx.x; i < end; i += 256) to[i] = from[i];
+}
+
+hipError_t launch_copy_runs(const void* src, void* dst, int n_runs, int per_group, const CopyStrides& st,
+                            size_t run_bytes, hipStream_t s) {
+  if (n_runs <= 0 || run_bytes == 0) return hipSuccess;
+  if (run_bytes % 16 || (uintptr_t)src % 16 || (uintptr_t)dst % 16 || st.src_group % 16 || st.src_run % 16 ||
+      st.dst_group % 16 || st.dst_run % 16 || per_group <= 0)
+    return hipErrorInvalidValue;
+  const size_t chunks = (run_bytes / 16 + 4095) / 4096;
+  if (chunks > 65535) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(run_copy_kernel, dim3(n_runs, (unsigned)chunks), dim3(256), 0, s, (const char*)src, (char*)dst,
+                     per_group, st, run_bytes);
+  return hipGetLastError();
 }
 
 hipError_t launch_run_copy(void* base, size_t src, size_t dst, int n_runs, int per_group, size_t group_stride,
                            size_t run_stride, size_t run_bytes, hipStream_t s) {
-  if (n_runs <= 0 || run_bytes == 0) return hipSuccess;
-  if (run_bytes % 16 || src % 16 || dst % 16 || group_stride % 16 || run_stride % 16 || per_group <= 0)
-    return hipErrorInvalidValue;
-  hipLaunchKernelGGL(run_copy_kernel, dim3(n_runs), dim3(256), 0, s, (char*)base, src, dst, per_group, group_stride,
-                     run_stride, run_bytes);
-  return hipGetLastError();
+  const CopyStrides st{group_stride, run_stride, group_stride, run_stride};
+  return launch_copy_runs((const char*)base + src, (char*)base + dst, n_runs, per_group, st, run_bytes, s);
 }
 
 // ------------------------------------------------------------------ weight repacking

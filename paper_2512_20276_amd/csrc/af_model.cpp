@@ -453,13 +453,14 @@ af_status with_splits(af_weights* w, GemmArgs& g) {
   return AF_OK;
 }
 
-af_status step_qkv(af_weights* w, int l, const void* xn, int ldx, long xs, int M, af_ring* ring, const DevTables& t,
+// l: the weights' layer; rl: the ring layer that holds this layer's keys and values.
+af_status step_qkv(af_weights* w, int l, const void* xn, int ldx, long xs, int M, af_ring* ring, int rl, const DevTables& t,
                    void* q_out, int ldq, hipStream_t s) {
   const af_model_desc& d = w->d;
   GemmArgs g = gemm_args(d.dtype, xn, ldx, xs, w->layers[l].wqkv, M, 3 * d.d_model, d.d_model, q_out, ldq);
   const size_t es = w->es;
-  g.ring_k = (char*)ring->kv + ring->offset(l, 0, 0, 0, 0) * es;
-  g.ring_v = (char*)ring->kv + ring->offset(l, 1, 0, 0, 0) * es;
+  g.ring_k = (char*)ring->kv + ring->offset(rl, 0, 0, 0, 0) * es;
+  g.ring_v = (char*)ring->kv + ring->offset(rl, 1, 0, 0, 0) * es;
   g.row_sp = t.row_sp;
   g.rope_cs = w->rope_cs;
   g.d_model = d.d_model;
@@ -546,14 +547,16 @@ af_status step_norm(af_weights* w, const void* x, int ldx, const int32_t* rows, 
 // One decoder layer (Alg. 2).  xn_ready: the previous layer's down projection already wrote
 // this layer's attention-normed rows into w->xn.  next_norm: the next layer's attention-norm
 // gain, which this layer's down projection applies when it can (*next_ready then says so).
-af_status layer_forward(af_weights* w, int l, void* hidden, int M, af_ring* ring, const DevTables& t, hipStream_t s,
-                        bool xn_ready = false, const void* next_norm = nullptr, bool* next_ready = nullptr) {
+// Layer l of the weights; its keys and values live in ring layer rl.
+af_status layer_forward(af_weights* w, int l, void* hidden, int M, af_ring* ring, int rl, const DevTables& t,
+                        hipStream_t s, bool xn_ready = false, const void* next_norm = nullptr,
+                        bool* next_ready = nullptr) {
   const Layer& L = w->layers[l];
   const int D = w->d.d_model, ldD = w->ldD, ldF = w->ldF;
   const long xD = w->xs_D, xF = w->xs_F;  // 0 (row-major) for fp32
   if (!xn_ready) AF_TRY(step_norm(w, hidden, D, nullptr, L.attn_norm, w->xn, ldD, xD, M, s));
-  AF_TRY(step_qkv(w, l, w->xn, ldD, xD, M, ring, t, w->q, ldD, s));
-  AF_TRY(step_attention(w, w->d.dtype, ring, l, w->q, ldD, w->attn, ldD, xD, t, s));
+  AF_TRY(step_qkv(w, l, w->xn, ldD, xD, M, ring, rl, t, w->q, ldD, s));
+  AF_TRY(step_attention(w, w->d.dtype, ring, rl, w->q, ldD, w->attn, ldD, xD, t, s));
   // InPlaceKVShift: no device work; the slot rotation lives in the ring bookkeeping.
   bool mlp_normed = false;
   AF_TRY(step_o(w, l, w->attn, ldD, xD, hidden, M, s, L.mlp_norm, &mlp_normed));
@@ -776,7 +779,7 @@ extern "C" af_status af_packed_forward(af_weights* w, const int32_t* token_ids, 
   for (int l = 0; l < d.n_layers; ++l) {
     const void* next = l + 1 < d.n_layers ? w->layers[l + 1].attn_norm : nullptr;
     bool next_ready = false;
-    AF_TRY(layer_forward(w, l, out_hidden, M, ring, t, s, xn_ready, next, &next_ready));
+    AF_TRY(layer_forward(w, l, out_hidden, M, ring, l, t, s, xn_ready, next, &next_ready));
     xn_ready = next_ready;
   }
   return lm_head(w, out_hidden, t, out_logits, out_tokens, s);
@@ -784,6 +787,13 @@ extern "C" af_status af_packed_forward(af_weights* w, const int32_t* token_ids, 
 
 extern "C" af_status af_packed_layer_forward(af_weights* w, int32_t layer, void* hidden_inout, int32_t M,
                                              const af_segment* segs, int32_t n_seg, af_ring* ring, void* hip_stream) {
+  clear_error();
+  return af_packed_layer_forward_kv(w, layer, hidden_inout, M, segs, n_seg, ring, layer, hip_stream);
+}
+
+extern "C" af_status af_packed_layer_forward_kv(af_weights* w, int32_t layer, void* hidden_inout, int32_t M,
+                                                const af_segment* segs, int32_t n_seg, af_ring* ring,
+                                                int32_t ring_layer, void* hip_stream) {
   clear_error();
   if (!w || !hidden_inout) {
     set_error("af_packed_layer_forward: weights and hidden must be non-NULL");
@@ -793,10 +803,14 @@ extern "C" af_status af_packed_layer_forward(af_weights* w, int32_t layer, void*
     set_error("af_packed_layer_forward: layer %d outside [0, %d)", layer, w->d.n_layers);
     return AF_ERR_OUT_OF_RANGE;
   }
+  if (ring_layer < 0) {
+    set_error("af_packed_layer_forward: ring layer %d is negative", ring_layer);
+    return AF_ERR_OUT_OF_RANGE;
+  }
   hipStream_t s = (hipStream_t)hip_stream;
   StepDesc sd;
-  AF_TRY(prepare_step(w, ring, segs, n_seg, M, layer + 1, sd, s));
-  return layer_forward(w, layer, hidden_inout, M, ring, dev_tables(w, sd), s);
+  AF_TRY(prepare_step(w, ring, segs, n_seg, M, ring_layer + 1, sd, s));
+  return layer_forward(w, layer, hidden_inout, M, ring, ring_layer, dev_tables(w, sd), s);
 }
 
 // ================================================================ single steps
@@ -896,7 +910,7 @@ extern "C" af_status af_op_qkv_rope_write(af_weights* w, int32_t layer, const vo
   StepDesc sd;
   AF_TRY(prepare_step(w, ring, segs, n_seg, M, layer + 1, sd, s));
   AF_TRY(stage_input(w, xn, w->d.d_model, M, w->xn, w->xs_D, s));
-  return step_qkv(w, layer, xn, w->d.d_model, w->xs_D, M, ring, dev_tables(w, sd), q_out, w->d.d_model, s);
+  return step_qkv(w, layer, xn, w->d.d_model, w->xs_D, M, ring, layer, dev_tables(w, sd), q_out, w->d.d_model, s);
 }
 
 extern "C" af_status af_op_attention(af_ring* ring, int32_t layer, const void* q, int32_t M, const af_segment* segs,

@@ -280,3 +280,25 @@ extern "C" af_status af_ring_read_kv(af_ring* ring, int32_t layer, int32_t slot,
   AF_TRY(ring_region_check(ring, layer, slot, pos0, n, k, v, "af_ring_read_kv"));
   return ring_copy(ring, layer, slot, pos0, n, k, v, false, (hipStream_t)hip_stream);
 }
+
+extern "C" af_status af_ring_copy_kv(const af_ring* src, int32_t src_layer, int32_t src_slot, af_ring* dst,
+                                     int32_t dst_layer, int32_t dst_slot, int32_t pos0, int32_t n, void* hip_stream) {
+  clear_error();
+  const int dummy = 0;
+  AF_TRY(ring_region_check(src, src_layer, src_slot, pos0, n, &dummy, &dummy, "af_ring_copy_kv (source)"));
+  AF_TRY(ring_region_check(dst, dst_layer, dst_slot, pos0, n, &dummy, &dummy, "af_ring_copy_kv (destination)"));
+  if (src->d.n_kv_heads != dst->d.n_kv_heads || src->d.head_dim != dst->d.head_dim || src->d.dtype != dst->d.dtype) {
+    set_error("af_ring_copy_kv: rings differ in heads, head_dim or dtype");
+    return AF_ERR_INVALID_ARG;
+  }
+  if (src == dst && src_layer == dst_layer && src_slot == dst_slot) return AF_OK;  // the region onto itself
+  const size_t es = dtype_size(src->d.dtype);
+  const int H = src->d.n_kv_heads, hd = src->d.head_dim;
+  // runs (kv, head): positions [pos0, pos0 + n) of one head are contiguous in a ring
+  const CopyStrides st{(src->offset(0, 1, 0, 0, 0) - src->offset(0, 0, 0, 0, 0)) * es, (size_t)src->d.max_pos * hd * es,
+                       (dst->offset(0, 1, 0, 0, 0) - dst->offset(0, 0, 0, 0, 0)) * es, (size_t)dst->d.max_pos * hd * es};
+  const char* from = (const char*)src->kv + src->offset(src_layer, 0, src_slot, 0, pos0) * es;
+  char* to = (char*)dst->kv + dst->offset(dst_layer, 0, dst_slot, 0, pos0) * es;
+  AF_HIP(launch_copy_runs(from, to, 2 * H, H, st, (size_t)n * hd * es, (hipStream_t)hip_stream));
+  return AF_OK;
+}

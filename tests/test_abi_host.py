@@ -221,3 +221,15 @@ def test_copy_shift_errors_leave_state_unchanged():
     ring.shift_stages(4)
     model.shift_stages(4)
     assert ring.state() == model.state() == ([-1, 0, 1, 2], [0, 2, 2, 2], 0)
+
+
+def test_kv_copy_and_ring_layer_calls_reject_bad_arguments_on_the_host():
+    """The naive pipeline's region copy and the ring-layer forward validate before any launch:
+    a bookkeeping-only ring has no storage, NULL handles are refused."""
+    a, b = af.Ring(0, 4, 16), af.Ring(0, 2, 16)
+    with pytest.raises(af.AFError) as e:
+        a.copy_kv_to(0, 0, b, 0, 0, 0, 4)
+    assert e.value.code == af.AF_ERR_INVALID_ARG and "storage" in str(e.value)
+    assert af.lib.af_ring_copy_kv(None, 0, 0, b.h, 0, 0, 0, 1, None) == af.AF_ERR_INVALID_ARG
+    assert af.lib.af_packed_layer_forward_kv(None, 0, None, 1, None, 0, a.h, 0, None) == af.AF_ERR_INVALID_ARG
+    assert a.state() == ([-1] * 4, [0] * 4, 0)
