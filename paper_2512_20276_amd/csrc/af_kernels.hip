@@ -732,6 +732,152 @@ __global__ __launch_bounds__(256, 1) void gemm32x2_kernel(GemmArgs a) {
   }
 }
 
+// Six-wave variant for 161..320 rows split two ways over K (the QKV projection's shape): the
+// tile is 160 rows x 192 columns, each wave owning one 32-column weight block over all five
+// row blocks, so no weight fragment is loaded twice and 2 x N / 192 x 2 workgroups fill the
+// GPU where 288 x 128 tiles leave a quarter of it idle.  Activations go through the LDS ring
+// by DMA issued by waves 0..3 (waves 4 and 5 issue none; every wave waits for its own loads and
+// then the barrier), the weights stream into per-wave register rings as in gemm32x2_kernel.
+// Split-K only: the kernel writes fp32 partial sums and splitk_reduce_kernel applies the epilogue.
+template <int FM, int NW>
+__global__ __launch_bounds__(64 * NW, 1) void gemm32c_kernel(GemmArgs a) {
+  constexpr int KS = 4, NBUF = 4, PFB = 8, BLK = 512;
+  constexpr int SB = FM * KS;  // fragment blocks per stage
+  constexpr int DW = SB / 4;   // DMAs per stage of each of waves 0..3
+  constexpr int P = PFB / KS;  // stages of weight lookahead
+  constexpr int TC = 32 * NW;  // tile columns
+  static_assert(NW >= 4 && SB % 4 == 0 && (NBUF * KS) % PFB == 0 && P >= 1, "pipeline shape");
+  constexpr int AS_BYTES = NBUF * SB * BLK * 2, T_BYTES = 32 * FM * TC * 4;
+  __shared__ __attribute__((aligned(1024))) char smem[AS_BYTES > T_BYTES ? AS_BYTES : T_BYTES];
+  bf16(*As)[SB * BLK] = (bf16(*)[SB * BLK])smem;
+  float* T_ = (float*)smem;  // the fp32 tile [32 FM][TC] once the main loop is done
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n_blocks = (a.N + 31) >> 5, n_nt = (n_blocks + NW - 1) / NW;
+  const int m_blocks = (a.M + 31) >> 5, n_mt = (m_blocks + FM - 1) / FM;
+  const int S = a.splits;
+  const int t = xcd_remap(blockIdx.x, n_mt * n_nt * S);
+  const int mt = t % n_mt, rest = t / n_mt;
+  const int sp = rest % S, nt = rest / S;
+  const int ks16 = a.Kp >> 4;
+  const int units = ks16 / (KS * NBUF), per = (units + S - 1) / S;
+  const int kb = min(units, sp * per) * (KS * NBUF), ke = min(units, sp * per + per) * (KS * NBUF);
+  const int n_st = (ke - kb) / KS;  // a multiple of NBUF
+  // this wave's weight block (past N: a valid block whose columns are never stored)
+  const bf16* bp = (const bf16*)a.B + (size_t)min(nt * NW + wave, n_blocks - 1) * a.bstride + lane * 8;
+  const bf16* __restrict__ Ab = (const bf16*)a.A;
+
+  auto body = [&](auto d_c) {
+    constexpr int D = decltype(d_c)::value;  // DMAs per stage issued by this wave
+    auto dma = [&](auto buf, int st) {
+      static_for<0, D>([&](auto d) {
+        const int q = wave + 4 * decltype(d)::value, mb = q / KS, j = q % KS;
+        const int k = min(kb + st * KS + j, ks16 - 1);
+        const int blk = min(mt * FM + mb, m_blocks - 1);  // rows past M: a valid block, never stored
+        const bf16* src = Ab + (size_t)blk * a.astride + (size_t)k * BLK + lane * 8;
+        __builtin_amdgcn_global_load_lds((const void*)src,
+                                         (__attribute__((address_space(3))) void*)&As[buf][q * BLK], 16, 0, 0);
+      });
+    };
+    bf16x8 rb[PFB];
+    auto load_b = [&](auto slot, int st, int j) {
+      const int k = min(kb + st * KS + j, ks16 - 1);
+      const bf16* src = bp + (size_t)k * BLK;
+      bf16x8 v;
+      asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(src) : "memory");
+      rb[slot] = v;
+    };
+    f32x16 acc[FM];
+    static_for<0, FM>([&](auto i) { acc[i] = f32x16{}; });
+    static_for<0, NBUF - 1>([&](auto b) {
+      dma(b, b);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    static_for<0, P>([&](auto s) {
+      static_for<0, KS>([&](auto j) { load_b(std::integral_constant<int, s * KS + j>{}, s, j); });
+    });
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the loop's waits count from a full ring
+    __builtin_amdgcn_sched_barrier(0);
+    for (int st0 = 0; st0 < n_st; st0 += NBUF) {
+      static_for<0, NBUF>([&](auto u) {
+        constexpr int U = decltype(u)::value;
+        const int st = st0 + U;
+        // stage st needs its weights (the last loads of stage st - P) and activations (the DMA
+        // of stage st - NBUF + 1); loads complete in order.  Per stage: D DMAs, then KS loads.
+        constexpr int WAIT = P <= NBUF - 1 ? (P - 1) * (D + KS) : KS + (NBUF - 2) * (D + KS);
+        static_assert(WAIT <= 63, "vmcnt range");
+        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(WAIT) : "memory");
+        dma(std::integral_constant<int, (U + NBUF - 1) % NBUF>{}, st + NBUF - 1);
+        __builtin_amdgcn_sched_barrier(0);
+        bf16x8 af[2][FM];
+        static_for<0, FM>([&](auto i) {
+          af[0][i] = *(const bf16x8*)(&As[U][(decltype(i)::value * KS) * BLK + lane * 8]);
+        });
+        static_for<0, KS>([&](auto j) {
+          constexpr int J = decltype(j)::value;
+          constexpr int slot = (U * KS + J) % PFB;
+          if constexpr (J + 1 < KS) {
+            static_for<0, FM>([&](auto i) {
+              af[(J + 1) & 1][i] = *(const bf16x8*)(&As[U][(decltype(i)::value * KS + J + 1) * BLK + lane * 8]);
+            });
+          }
+          __builtin_amdgcn_sched_barrier(0);
+          static_for<0, FM>([&](auto i) {
+            acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[J & 1][i], rb[slot], acc[i], 0, 0, 0);
+          });
+          load_b(std::integral_constant<int, slot>{}, st + P, J);
+          __builtin_amdgcn_sched_barrier(0);
+        });
+      });
+    }
+    // the ring's last (unused) loads land before any of its registers can be reused
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+#pragma unroll
+    for (int p = 0; p < PFB; ++p) asm volatile("" : "+v"(rb[p]));
+    __syncthreads();  // every wave's DMAs have landed and its LDS reads are done
+    static_for<0, FM>([&](auto i) {
+      static_for<0, 16>([&](auto r) {
+        constexpr int R = decltype(r)::value;
+        const int row = (int)decltype(i)::value * 32 + 8 * (R / 4) + 4 * (lane >> 5) + (R % 4);
+        T_[row * TC + wave * 32 + (lane & 31)] = acc[i][R];
+      });
+    });
+  };
+  if (wave < 4)
+    body(std::integral_constant<int, DW>{});
+  else
+    body(std::integral_constant<int, 0>{});
+  __syncthreads();
+
+  // ---------------- the fp32 partial sums of split sp, 8 columns per item
+  constexpr int ITEMS = 32 * FM * (TC / 8);
+  const int m0 = mt * FM * 32, n0 = nt * TC;
+  for (int it = tid; it < ITEMS; it += 64 * NW) {
+    const int row = it / (TC / 8), col = (it % (TC / 8)) * 8;
+    const int m = m0 + row, nc = n0 + col;
+    if (m >= a.M || nc >= a.N) continue;  // N % 8 == 0: a group is wholly inside or outside
+    float* dst = a.partial + ((size_t)sp * a.M + m) * a.N + nc;
+    *(f32x4*)dst = *(const f32x4*)&T_[row * TC + col];
+    *(f32x4*)(dst + 4) = *(const f32x4*)&T_[row * TC + col + 4];
+  }
+}
+
+// The six-wave tile is taken for a two-way K split of 161..320 rows when it fills 3/4 of the
+// GPU or more in one pass (the QKV projection of a 7B-shape step: 2 x 64 x 2 = 256 workgroups).
+constexpr int C6_FM = 5, C6_NW = 6;
+static bool use_c6(const GemmArgs& a) {
+  const int mb = (a.M + 31) / 32, nb = (a.N + 31) / 32;
+  const int wgs = ((mb + C6_FM - 1) / C6_FM) * ((nb + C6_NW - 1) / C6_NW) * a.splits;
+  return a.splits == 2 && mb > C6_FM && mb <= 2 * C6_FM && wgs >= 192 && wgs <= 256;
+}
+
+static hipError_t gemm32c_launch(const GemmArgs& a, hipStream_t s) {
+  const int mb = (a.M + 31) / 32, nb = (a.N + 31) / 32;
+  const dim3 grid(((mb + C6_FM - 1) / C6_FM) * ((nb + C6_NW - 1) / C6_NW) * a.splits);
+  hipLaunchKernelGGL((gemm32c_kernel<C6_FM, C6_NW>), grid, dim3(64 * C6_NW), 0, s, a);
+  return hipGetLastError();
+}
+
 // 32-row blocks per tile: the smallest tile that holds every row (up to 10 blocks, 320 rows;
 // FM = 10 fills the 160 KB of LDS), else the tile of 9 or 10 blocks with the fewest tiles and
 // then the least padding.  A row's accumulation order is the same in every tile shape.
@@ -774,6 +920,11 @@ static hipError_t gemm_dispatch_bf16(int epi, const GemmArgs& a, hipStream_t s) 
   if (a.astride <= 0 || a.Kp % 256 != 0 || a.astride < (long)a.Kp * 32 || a.bstride < (long)a.Kp * 32)
     return hipErrorInvalidValue;
   hipError_t e;
+  if (use_c6(a)) {
+    e = gemm32c_launch(a, s);
+    if (e != hipSuccess || a.partials_only) return e;
+    return reduce_launch<bf16>(epi, a, s);
+  }
   switch (fm_for(a.M)) {
     case 1: e = gemm32_launch<1, false>(epi, a, s); break;
     case 3: e = gemm32_launch<3, true>(epi, a, s); break;

@@ -71,6 +71,20 @@ def test_linear(storage, M, N, K):
                   rtol=8e-3 if storage == "bf16" else 1e-5)
 
 
+@pytest.mark.parametrize("M", [161, 200, 282, 291, 320])
+def test_linear_qkv_width_split_k(M):
+    """N = 12288, K = 4096 (the QKV projection's width) at 161..320 rows: a two-way K split on the
+    six-wave 160 x 192 tile, two row tiles, ragged rows; partial sums and reduce against fp64."""
+    N, K = 12288, 4096
+    x = wl.draw(("t_lin_x", M, K), (M, K), device="cuda")
+    w = wl.draw(("t_lin_w", N, K), (N, K), std=0.02, device="cuda")
+    y = torch.full((M, N), float("nan"), dtype=torch.bfloat16, device="cuda")
+    af.op_linear(x, w, y)
+    torch.cuda.synchronize()
+    ref = round_storage(linear(to_np(x), to_np(w)), "bf16")
+    _assert_close(y, ref, "bf16", "linear", min_exact=0.99, atol=1e-3, rtol=8e-3)
+
+
 def test_linear_large_m():
     """M = 2264 (eight 283-row pipelines), several M tiles and a ragged tail."""
     M, N, K = 2264, 512, 4096
