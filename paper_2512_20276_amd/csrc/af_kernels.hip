@@ -864,18 +864,20 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm32c_kernel(GemmArgs a) {
 
 // The six-wave tile is taken at 161..320 rows for a two-way K split when it fills 3/4 of the
 // GPU or more in one pass (the QKV projection of a 7B-shape step: 2 x 64 x 2 = 256 workgroups),
-// and for the four-way split planned for narrow projections with K <= 4096 (the output
-// projection: 2 x 22 x 4 = 176 workgroups, half the partial sums of the 8-way split that the
-// 288 x 128 tile needs to fill the GPU).
+// and for narrow projections (N <= 4224) split four ways for K <= 4096, five ways beyond (the
+// output and down projections: 2 x 22 x 4 = 176 and 2 x 22 x 5 = 220 workgroups), which write
+// about half the fp32 partial sums of the 8-way split the 288 x 128 tile needs to fill the GPU.
 constexpr int C6_FM = 5, C6_NW = 6;
-static bool c6_narrow(int M, int N, int Kp) {
-  const int mb = (M + 31) / 32, nb = (N + 31) / 32;
-  return mb > C6_FM && mb <= 2 * C6_FM && nb <= 132 && Kp <= 4096 && Kp / 256 >= 4;
+static int c6_narrow(int M, int N, int Kp) {
+  const int mb = (M + 31) / 32, nb = (N + 31) / 32, units = Kp / 256;
+  if (mb <= C6_FM || mb > 2 * C6_FM || nb > 132 || units < 4) return 0;
+  const int S = Kp <= 4096 ? 4 : 5, per = (units + S - 1) / S;
+  return (units + per - 1) / per;
 }
 static bool use_c6(const GemmArgs& a) {
   const int mb = (a.M + 31) / 32, nb = (a.N + 31) / 32;
   const int wgs = ((mb + C6_FM - 1) / C6_FM) * ((nb + C6_NW - 1) / C6_NW) * a.splits;
-  if (a.splits == 4 && c6_narrow(a.M, a.N, a.Kp)) return true;
+  if (a.splits > 1 && a.splits == c6_narrow(a.M, a.N, a.Kp)) return true;
   return a.splits == 2 && mb > C6_FM && mb <= 2 * C6_FM && wgs >= 192 && wgs <= 256;
 }
 
@@ -947,7 +949,7 @@ static hipError_t gemm_dispatch_bf16(int epi, const GemmArgs& a, hipStream_t s) 
 
 int gemm_splits(int dtype, int M, int N, int Kp) {
   if (dtype == AF_BF16) {
-    if (c6_narrow(M, N, Kp)) return 4;
+    if (const int S = c6_narrow(M, N, Kp)) return S;
     const int fm = fm_for(M);
     const int tiles = (((M + 31) / 32 + fm - 1) / fm) * (((N + 31) / 32 + 3) / 4);
     return splits_for(tiles, Kp / gemm_k_align());
