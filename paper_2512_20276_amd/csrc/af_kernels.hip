@@ -732,14 +732,15 @@ __global__ __launch_bounds__(256, 1) void gemm32x2_kernel(GemmArgs a) {
   }
 }
 
-// Six-wave variant for 161..320 rows split two ways over K (the QKV projection's shape): the
-// tile is 160 rows x 192 columns, each wave owning one 32-column weight block over all five
-// row blocks, so no weight fragment is loaded twice and 2 x N / 192 x 2 workgroups fill the
-// GPU where 288 x 128 tiles leave a quarter of it idle.  Activations go through the LDS ring
+// Six-wave variant for 161..320 rows: the tile is 160 rows x 192 columns, each wave owning one
+// 32-column weight block over all five row blocks, so no weight fragment is loaded twice and
+// 2 x N / 192 workgroups (times the K split) fill the GPU where 288 x 128 tiles leave a quarter
+// of it idle.  Activations go through the LDS ring
 // by DMA issued by waves 0..3 (waves 4 and 5 issue none; every wave waits for its own loads and
 // then the barrier), the weights stream into per-wave register rings as in gemm32x2_kernel.
-// Split-K only: the kernel writes fp32 partial sums and splitk_reduce_kernel applies the epilogue.
-template <int FM, int NW>
+// With a K split the kernel writes fp32 partial sums and splitk_reduce_kernel applies the
+// epilogue; unsplit it applies the epilogue itself.
+template <int FM, int NW, int EPI>
 __global__ __launch_bounds__(64 * NW, 1) void gemm32c_kernel(GemmArgs a) {
   constexpr int KS = 4, NBUF = 4, PFB = 8, BLK = 512;
   constexpr int SB = FM * KS;  // fragment blocks per stage
@@ -849,21 +850,33 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm32c_kernel(GemmArgs a) {
     body(std::integral_constant<int, 0>{});
   __syncthreads();
 
-  // ---------------- the fp32 partial sums of split sp, 8 columns per item
-  constexpr int ITEMS = 32 * FM * (TC / 8);
+  // ---------------- epilogue over the fp32 tile (as in gemm32_kernel)
+  constexpr bool paired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
+  constexpr int W = paired ? 16 : 8;
+  constexpr int ITEMS = 32 * FM * (TC / W);
   const int m0 = mt * FM * 32, n0 = nt * TC;
   for (int it = tid; it < ITEMS; it += 64 * NW) {
-    const int row = it / (TC / 8), col = (it % (TC / 8)) * 8;
+    const int row = it / (TC / W), col = (it % (TC / W)) * W;
     const int m = m0 + row, nc = n0 + col;
-    if (m >= a.M || nc >= a.N) continue;  // N % 8 == 0: a group is wholly inside or outside
-    float* dst = a.partial + ((size_t)sp * a.M + m) * a.N + nc;
-    *(f32x4*)dst = *(const f32x4*)&T_[row * TC + col];
-    *(f32x4*)(dst + 4) = *(const f32x4*)&T_[row * TC + col + 4];
+    if (m >= a.M || nc >= a.N) continue;  // N % 16 == 0: a group is wholly inside or outside
+    float v[W];
+#pragma unroll
+    for (int e = 0; e < W; e += 4) *(f32x4*)&v[e] = *(const f32x4*)&T_[row * TC + col + e];
+    if (S > 1) {
+      float* dst = a.partial + ((size_t)sp * a.M + m) * a.N + nc;
+#pragma unroll
+      for (int e = 0; e < W; e += 4) *(f32x4*)(dst + e) = *(const f32x4*)&v[e];
+    } else if constexpr (paired) {
+      epi_group16<bf16, EPI>(a, m, nc, v, v + 8);
+    } else {
+      epi_group8<bf16, EPI>(a, m, nc, v);
+    }
   }
 }
 
-// The six-wave tile is taken at 161..320 rows for a two-way K split when it fills 3/4 of the
-// GPU or more in one pass (the QKV projection of a 7B-shape step: 2 x 64 x 2 = 256 workgroups),
+// The six-wave tile is taken at 161..320 rows, unsplit or split two ways over K, when it fills
+// 3/4 of the GPU or more in one pass (a 7B-shape step's gate/up projection: 2 x 115 = 230
+// workgroups; its QKV projection: 2 x 64 x 2 = 256),
 // and for narrow projections (N <= 4224) split four ways for K <= 4096, five ways beyond (the
 // output and down projections: 2 x 22 x 4 = 176 and 2 x 22 x 5 = 220 workgroups), which write
 // about half the fp32 partial sums of the 8-way split the 288 x 128 tile needs to fill the GPU.
@@ -878,13 +891,24 @@ static bool use_c6(const GemmArgs& a) {
   const int mb = (a.M + 31) / 32, nb = (a.N + 31) / 32;
   const int wgs = ((mb + C6_FM - 1) / C6_FM) * ((nb + C6_NW - 1) / C6_NW) * a.splits;
   if (a.splits > 1 && a.splits == c6_narrow(a.M, a.N, a.Kp)) return true;
-  return a.splits == 2 && mb > C6_FM && mb <= 2 * C6_FM && wgs >= 192 && wgs <= 256;
+  return a.splits <= 2 && mb > C6_FM && mb <= 2 * C6_FM && wgs >= 192 && wgs <= 256;
 }
 
-static hipError_t gemm32c_launch(const GemmArgs& a, hipStream_t s) {
+static hipError_t gemm32c_launch(int epi, const GemmArgs& a, hipStream_t s) {
   const int mb = (a.M + 31) / 32, nb = (a.N + 31) / 32;
-  const dim3 grid(((mb + C6_FM - 1) / C6_FM) * ((nb + C6_NW - 1) / C6_NW) * a.splits);
-  hipLaunchKernelGGL((gemm32c_kernel<C6_FM, C6_NW>), grid, dim3(64 * C6_NW), 0, s, a);
+  const dim3 grid(((mb + C6_FM - 1) / C6_FM) * ((nb + C6_NW - 1) / C6_NW) * a.splits), block(64 * C6_NW);
+  if (a.splits > 1) {  // partial sums only: one instance serves every epilogue
+    hipLaunchKernelGGL((gemm32c_kernel<C6_FM, C6_NW, EPI_STORE>), grid, block, 0, s, a);
+    return hipGetLastError();
+  }
+  switch (epi) {
+    case EPI_STORE: hipLaunchKernelGGL((gemm32c_kernel<C6_FM, C6_NW, EPI_STORE>), grid, block, 0, s, a); break;
+    case EPI_STORE_F32: hipLaunchKernelGGL((gemm32c_kernel<C6_FM, C6_NW, EPI_STORE_F32>), grid, block, 0, s, a); break;
+    case EPI_RESID: hipLaunchKernelGGL((gemm32c_kernel<C6_FM, C6_NW, EPI_RESID>), grid, block, 0, s, a); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm32c_kernel<C6_FM, C6_NW, EPI_SWIGLU>), grid, block, 0, s, a); break;
+    case EPI_QKV: hipLaunchKernelGGL((gemm32c_kernel<C6_FM, C6_NW, EPI_QKV>), grid, block, 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
@@ -931,8 +955,8 @@ static hipError_t gemm_dispatch_bf16(int epi, const GemmArgs& a, hipStream_t s) 
     return hipErrorInvalidValue;
   hipError_t e;
   if (use_c6(a)) {
-    e = gemm32c_launch(a, s);
-    if (e != hipSuccess || a.partials_only) return e;
+    e = gemm32c_launch(epi, a, s);
+    if (e != hipSuccess || a.splits <= 1 || a.partials_only) return e;
     return reduce_launch<bf16>(epi, a, s);
   }
   switch (fm_for(a.M)) {
