@@ -87,16 +87,18 @@ def measured_traffic():
 def _kernel_class(name: str) -> str:
     """Maps a kernel name (mangled or demangled) to the label used in the summaries."""
     import re
-    if "gemm_kernel" in name or "gemm32_kernel" in name or "gemm32x2_kernel" in name:
-        epi = (re.search(r"gemm32(?:x2)?_kernelI(?:Li\d+E)*Li(\d+)EEEv", name)      # bf16, mangled
-               or re.search(r"gemm32(?:x2)?_kernel<[^>]*?(\d+)>", name)              # bf16, demangled
+    if any(k in name for k in ("gemm_kernel", "gemm32_kernel", "gemm32x2_kernel", "gemm32c_kernel")):
+        epi = (re.search(r"gemm32(?:x2|c)?_kernelI(?:Li\d+E)*Li(\d+)EEEv", name)    # bf16, mangled
+               or re.search(r"gemm32(?:x2|c)?_kernel<[^>]*?(\d+)>", name)            # bf16, demangled
                or re.search(r",\s*(\d)>\s*\(", name) or re.search(r",\s*\(af::Epi\)(\d)>", name)
                or re.search(r"GemmCfgI(?:Li\d+E)+EELi(\d)E", name))                  # fp32 kernel
         e = int(epi.group(1)) if epi else -1
+        if "gemm32c_kernel" in name and e == 0:  # its split-K instance: partial sums only
+            return "gemm (split-K partials: QKV / O / down)"
         return {0: "gemm (store)", 1: "gemm (f32 store, LM head)", 2: "gemm (+residual: O / down)",
                 3: "gemm (gate/up + SwiGLU)", 4: "gemm (QKV + RoPE + ring write)"}.get(e, "gemm")
-    for key in ("splitk_reduce", "attention_kernel", "rmsnorm_kernel", "embed_kernel", "argmax_kernel",
-                "frag_pack_kernel"):
+    for key in ("splitk_reduce", "resid_norm_kernel", "attention_kernel", "rmsnorm_kernel", "embed_kernel",
+                "argmax_kernel", "frag_pack_kernel"):
         if key in name:
             return key
     if "neg" in name.lower():

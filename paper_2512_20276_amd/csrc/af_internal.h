@@ -75,7 +75,7 @@ struct AttnArgs {
   const DevSeg* segs;
   const int32_t* tiles;  // [n_tiles][2]: (segment, first row in segment); multi-row tiles first
   int n_multi;           // tiles of segments with more than one row (the rest are single rows)
-  int tile_base;         // set by the launcher: work tile of blockIdx.x = tile_base + blockIdx.x
+  int n_tiles;           // set by the launcher: all tiles
   int n_heads, max_pos, ldq, ldo;  // row strides of q and o (>= H*hd)
   long ostride;              // > 0: o is written fragment-tiled (32-row blocks ostride apart)
   float scale_log2;          // log2(e) / sqrt(hd)

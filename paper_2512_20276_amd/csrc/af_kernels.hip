@@ -999,11 +999,11 @@ hipError_t launch_gemm(int dtype, int epi, const GemmArgs& a, hipStream_t s) {
 // each lane holds scores of one query and the probabilities feed the P.V MFMA as its B
 // operand without a lane exchange; softmax is online in the exp2 domain with the running
 // max reduced across the four lanes that share a query.
-// Single-row segments (decode steps), one workgroup per (segment, head): one query against
-// its slot's keys 0 .. pos0.  The four waves take chunks of 64 keys in turn.  A chunk issues all
-// of its loads first (one memory latency per chunk): lane l's key c*64 + l for the score, and
-// for the value sum VEC dims of one dim group (l % DG) over the keys of its key group
-// (l / DG + KG t), so every access is a 16-byte load.  Scores are fp32 dot products of the
+// Single-row segments (decode steps), two per workgroup and head, each on half of the waves:
+// one query against its slot's keys 0 .. pos0.  The waves of a half take chunks of 32 keys in
+// turn.  A chunk issues all of its loads first (one memory latency per chunk): two lanes per key
+// for the score (half a key row each), and for the value sum VEC dims of one dim group (l % DG)
+// over the keys of its key group (l / DG + KG t), so every access is a 16-byte load.  Scores are fp32 dot products of the
 // stored vectors (bf16 pairs through v_dot2); the softmax is online in the exp2 domain; the
 // waves' (max, sum, output) are merged through LDS.  Separate from the tiled kernel so each
 // keeps its own register budget.
@@ -1026,99 +1026,114 @@ __device__ __forceinline__ float dot_vec(const uint4& k, const uint4& q, float a
   }
 }
 
-template <typename T, int HD>
-__device__ __forceinline__ void attention_decode_row(const AttnArgs& a, int tile) {
+// ROWS (1 or 2) single-row segments per workgroup: tiles first .. first + ROWS - 1 (those that
+// exist), each on ATTN_WAVES / ROWS waves.  Two per workgroup halve the workgroups a packed
+// step's decode rows take next to its query tiles.  Either way a row is computed as ATTN_WAVES
+// virtual waves (virtual wave v takes chunks v, v + ATTN_WAVES, ..; a wave of a pair runs two
+// of them one after the other) merged in virtual-wave order, so the result does not depend on
+// how many rows share the workgroup.
+template <typename T, int HD, int ROWS>
+__device__ __forceinline__ void attention_decode_rows(const AttnArgs& a, int first) {
   constexpr int VEC = Chunk<T>::N;  // elements per 16 bytes
   constexpr int DG = HD / VEC;      // 16-byte chunks per key row
   constexpr int KH2 = DG / 2;       // chunks per half row (two lanes per key for the scores)
   constexpr int KG = 64 / DG;       // value key groups (lane / DG)
   constexpr int KPL = 32 / KG;      // values: keys per lane per 32-key chunk
   static_assert(DG % 2 == 0 && DG <= 64 && 64 % DG == 0 && 32 % KG == 0, "head_dim");
-  constexpr int NW = ATTN_WAVES;
-  __shared__ float wm[NW], wl[NW];
-  __shared__ __attribute__((aligned(16))) float wo[NW][HD];
-  __shared__ __attribute__((aligned(16))) uint4 qs[DG];
-  const int seg_i = a.tiles[2 * tile];
+  static_assert(ROWS == 1 || ROWS == 2, "rows per workgroup");
+  constexpr int VW = ATTN_WAVES;         // virtual waves per row
+  constexpr int NW = ATTN_WAVES / ROWS;  // waves per row
+  __shared__ float wm[ROWS][VW], wl[ROWS][VW];
+  __shared__ __attribute__((aligned(16))) float wo[ROWS][VW][HD];
+  __shared__ __attribute__((aligned(16))) uint4 qs[ROWS][DG];
+  const int tid = threadIdx.x, lane = tid & 63, wave0 = tid >> 6;
+  const int sub = ROWS == 1 ? 0 : wave0 / NW, wave = ROWS == 1 ? wave0 : wave0 % NW;  // row, wave within it
+  const bool live = ROWS == 1 || first + sub < a.n_tiles;  // an odd count leaves the last half idle
+  const int seg_i = a.tiles[2 * (live ? first + sub : first)];
   const int h = blockIdx.y;
   const DevSeg sg = a.segs[seg_i];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int kv_len = sg.pos0 + 1;
+  const int kv_len = live ? sg.pos0 + 1 : 0;
   const size_t slot_off = ((size_t)sg.slot * a.n_heads + h) * a.max_pos * HD;
   const T* __restrict__ Kg = (const T*)a.ring_k + slot_off;
   const T* __restrict__ Vg = (const T*)a.ring_v + slot_off;
-  // the query, the same for every lane, is read from LDS (broadcast reads)
-  if (tid < DG) qs[tid] = ((const uint4*)((const T*)a.q + (size_t)sg.q_start * a.ldq + h * HD))[tid];
+  // the query, the same for every lane of the row's waves, is read from LDS (broadcast reads)
+  const int htid = tid - sub * NW * 64;
+  if (live && htid < DG) qs[sub][htid] = ((const uint4*)((const T*)a.q + (size_t)sg.q_start * a.ldq + h * HD))[htid];
   __syncthreads();
 
   const int half = lane & 1, kl = lane >> 1;   // scores: key kl of the chunk, half row `half`
   const int dg = lane % DG, kgrp = lane / DG;  // values: dims [VEC dg, +VEC) of keys kgrp + KG t
-  float m_run = -INFINITY, l_run = 0.f, o[VEC];
 #pragma unroll
-  for (int e = 0; e < VEC; ++e) o[e] = 0.f;
-  for (int c = wave; c * 32 < kv_len; c += NW) {
-    // keys past kv_len read a clamped valid key and score -inf
-    const int j = c * 32 + kl;
-    const uint4* krow = (const uint4*)(Kg + (size_t)min(j, kv_len - 1) * HD) + half * KH2;
-    uint4 kv[KH2], vv[KPL];
+  for (int r = 0; r < VW / NW; ++r) {
+    const int v = wave + r * NW;  // the virtual wave
+    float m_run = -INFINITY, l_run = 0.f, o[VEC];
 #pragma unroll
-    for (int pc = 0; pc < KH2; ++pc) kv[pc] = krow[pc];
+    for (int e = 0; e < VEC; ++e) o[e] = 0.f;
+    for (int c = v; c * 32 < kv_len; c += VW) {
+      // keys past kv_len read a clamped valid key and score -inf
+      const int j = c * 32 + kl;
+      const uint4* krow = (const uint4*)(Kg + (size_t)min(j, kv_len - 1) * HD) + half * KH2;
+      uint4 kv[KH2], vv[KPL];
 #pragma unroll
-    for (int t = 0; t < KPL; ++t)
-      vv[t] = *(const uint4*)(Vg + (size_t)min(c * 32 + kgrp + KG * t, kv_len - 1) * HD + dg * VEC);
-    float dot = 0.f;
+      for (int pc = 0; pc < KH2; ++pc) kv[pc] = krow[pc];
 #pragma unroll
-    for (int pc = 0; pc < KH2; ++pc) dot = dot_vec<T>(kv[pc], qs[half * KH2 + pc], dot);
-    dot += __shfl_xor(dot, 1);
-    const float sc = j < kv_len ? dot * a.scale_log2 : -INFINITY;
-    float cm = sc;
+      for (int t = 0; t < KPL; ++t)
+        vv[t] = *(const uint4*)(Vg + (size_t)min(c * 32 + kgrp + KG * t, kv_len - 1) * HD + dg * VEC);
+      float dot = 0.f;
 #pragma unroll
-    for (int off = 32; off > 1; off >>= 1) cm = fmaxf(cm, __shfl_xor(cm, off));
-    const float m_new = fmaxf(m_run, cm);
-    const float p = exp2f(sc - m_new);
-    float ps = half ? 0.f : p;  // each key is held by two lanes
+      for (int pc = 0; pc < KH2; ++pc) dot = dot_vec<T>(kv[pc], qs[sub][half * KH2 + pc], dot);
+      dot += __shfl_xor(dot, 1);
+      const float sc = j < kv_len ? dot * a.scale_log2 : -INFINITY;
+      float cm = sc;
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) ps += __shfl_xor(ps, off);
-    const float corr = exp2f(m_run - m_new);  // 0 on the first chunk (m_run = -inf)
-    l_run = l_run * corr + ps;
-    m_run = m_new;
+      for (int off = 32; off > 1; off >>= 1) cm = fmaxf(cm, __shfl_xor(cm, off));
+      const float m_new = fmaxf(m_run, cm);
+      const float p = exp2f(sc - m_new);
+      float ps = half ? 0.f : p;  // each key is held by two lanes
 #pragma unroll
-    for (int e = 0; e < VEC; ++e) o[e] *= corr;
-    // lane covers dims [VEC dg, +VEC) of keys c*32 + kgrp + KG t (masked keys carry p = 0)
+      for (int off = 32; off > 0; off >>= 1) ps += __shfl_xor(ps, off);
+      const float corr = exp2f(m_run - m_new);  // 0 on the first chunk (m_run = -inf)
+      l_run = l_run * corr + ps;
+      m_run = m_new;
 #pragma unroll
-    for (int t = 0; t < KPL; ++t) {
-      const float pj = __shfl(p, 2 * (kgrp + KG * t));
-      T vt[VEC];
-      __builtin_memcpy(vt, &vv[t], 16);
+      for (int e = 0; e < VEC; ++e) o[e] *= corr;
+      // lane covers dims [VEC dg, +VEC) of keys c*32 + kgrp + KG t (masked keys carry p = 0)
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) o[e] += pj * to_f(vt[e]);
+      for (int t = 0; t < KPL; ++t) {
+        const float pj = __shfl(p, 2 * (kgrp + KG * t));
+        T vt[VEC];
+        __builtin_memcpy(vt, &vv[t], 16);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) o[e] += pj * to_f(vt[e]);
+      }
     }
+    // ---- merge the key groups of the virtual wave; park its state for the row's merge
+#pragma unroll
+    for (int off = DG; off < 64; off <<= 1)
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) o[e] += __shfl_xor(o[e], off);
+    if (lane == 0) {
+      wm[sub][v] = m_run;
+      wl[sub][v] = l_run;
+    }
+    if (lane < DG)
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) wo[sub][v][dg * VEC + e] = o[e];
   }
-  // ---- merge the key groups of the wave, then the four waves
-#pragma unroll
-  for (int off = DG; off < 64; off <<= 1)
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) o[e] += __shfl_xor(o[e], off);
-  if (lane == 0) {
-    wm[wave] = m_run;
-    wl[wave] = l_run;
-  }
-  if (lane < DG)
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) wo[wave][dg * VEC + e] = o[e];
   __syncthreads();
-  if (wave == 0 && lane < DG) {
-    float M = wm[0];
+  if (live && wave == 0 && lane < DG) {
+    float M = wm[sub][0];
 #pragma unroll
-    for (int w = 1; w < NW; ++w) M = fmaxf(M, wm[w]);
+    for (int w = 1; w < VW; ++w) M = fmaxf(M, wm[sub][w]);
     float L = 0.f, acc[VEC];
 #pragma unroll
     for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      const float f = wm[w] == -INFINITY ? 0.f : exp2f(wm[w] - M);  // a wave with no chunk holds nothing
-      L += wl[w] * f;
+    for (int w = 0; w < VW; ++w) {
+      const float f = wm[sub][w] == -INFINITY ? 0.f : exp2f(wm[sub][w] - M);  // a virtual wave with no chunk
+      L += wl[sub][w] * f;
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) acc[e] += wo[w][dg * VEC + e] * f;
+      for (int e = 0; e < VEC; ++e) acc[e] += wo[sub][w][dg * VEC + e] * f;
     }
     const float inv = 1.0f / L;
     T r[VEC];
@@ -1364,16 +1379,20 @@ __device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int ti
 
 // One launch for the whole step: work tiles [0, n_multi) are query tiles of multi-row segments
 // (ordered longest first, so they start first), the rest single-row segments.
+// Blocks [0, n_multi) of the query-tile instance take the query tiles, its other blocks pairs of
+// single-row tiles (n_multi + 2 (blockIdx.x - n_multi) and the next); the decode-only instance
+// takes one single-row tile per block (n_multi + blockIdx.x), on all of its waves.
 template <typename T, int HD, bool PREFILL>
 __global__ __launch_bounds__(64 * ATTN_WAVES, !PREFILL ? 4 : 2) void attention_kernel(AttnArgs a) {
-  const int tile = a.tile_base + blockIdx.x;
+  const int b = blockIdx.x;
   if constexpr (PREFILL) {
-    if (tile < a.n_multi) {
-      attention_prefill_tile<T, HD>(a, tile);
-      return;
-    }
+    if (b < a.n_multi)
+      attention_prefill_tile<T, HD>(a, b);
+    else
+      attention_decode_rows<T, HD, 2>(a, a.n_multi + 2 * (b - a.n_multi));
+  } else {
+    attention_decode_rows<T, HD, 1>(a, a.n_multi + b);
   }
-  attention_decode_row<T, HD>(a, tile);
 }
 
 // Query tiles and decode rows share one launch, query tiles first; the decode-only kernel has
@@ -1382,17 +1401,17 @@ __global__ __launch_bounds__(64 * ATTN_WAVES, !PREFILL ? 4 : 2) void attention_k
 template <typename T, int HD>
 static void attention_launch(const AttnArgs& a0, int n_tiles, hipStream_t s) {
   AttnArgs a = a0;
-  a.tile_base = 0;
+  a.n_tiles = n_tiles;
   const dim3 block(64 * ATTN_WAVES);
-  const int n_single = n_tiles - a.n_multi;
+  const int n_single = n_tiles - a.n_multi, n_pairs = (n_single + 1) / 2;
   if (a.n_multi == 0) {
     hipLaunchKernelGGL((attention_kernel<T, HD, false>), dim3(n_tiles, a.n_heads), block, 0, s, a);
-  } else if ((long)n_single * a.n_heads <= 512) {
-    hipLaunchKernelGGL((attention_kernel<T, HD, true>), dim3(n_tiles, a.n_heads), block, 0, s, a);
+  } else if ((long)n_pairs * a.n_heads <= 256) {
+    hipLaunchKernelGGL((attention_kernel<T, HD, true>), dim3(a.n_multi + n_pairs, a.n_heads), block, 0, s, a);
   } else {
     hipLaunchKernelGGL((attention_kernel<T, HD, true>), dim3(a.n_multi, a.n_heads), block, 0, s, a);
-    a.tile_base = a.n_multi;
-    hipLaunchKernelGGL((attention_kernel<T, HD, false>), dim3(n_single, a.n_heads), block, 0, s, a);
+    if (n_single > 0)  // the decode-only instance: its blocks start at the first single-row tile
+      hipLaunchKernelGGL((attention_kernel<T, HD, false>), dim3(n_single, a.n_heads), block, 0, s, a);
   }
 }
 
