@@ -1431,14 +1431,30 @@ hipError_t launch_attention(int dtype, int head_dim, const AttnArgs& a, int n_ti
 }
 
 // ------------------------------------------------------------------ RMSNorm
-// One workgroup of 256 threads per output row; rows[] optionally selects the input row.  The
+// One workgroup of NORM_THREADS threads per output row (a 4096-wide bf16 row is one 16-byte
+// chunk per thread: one memory latency); rows[] optionally selects the input row.  The
 // output is row-major (row stride ldy) or, with ystride > 0, fragment-tiled for the GEMM that
 // consumes it.  bf16 rows with D % 8 == 0 move 16 bytes per thread access.
+constexpr int NORM_THREADS = 512;
+
+// Sum over the workgroup of one value per thread, in a fixed order (lanes by xor shuffles, then
+// the waves in order); the same order in every kernel that normalises a row.
+__device__ __forceinline__ float norm_block_sum(float v, float* red) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  float tot = red[0];
+#pragma unroll
+  for (int w = 1; w < NORM_THREADS / 64; ++w) tot += red[w];
+  return tot;
+}
+
 template <typename T>
-__global__ __launch_bounds__(256) void rmsnorm_kernel(const T* __restrict__ x, int ldx, const int32_t* rows,
+__global__ __launch_bounds__(NORM_THREADS) void rmsnorm_kernel(const T* __restrict__ x, int ldx, const int32_t* rows,
                                                       const T* __restrict__ g, T* __restrict__ y, int ldy,
                                                       long ystride, int D, float eps) {
-  __shared__ float red[4];
+  __shared__ float red[NORM_THREADS / 64];
   const int r_out = blockIdx.x;
   const int r_in = rows ? rows[r_out] : r_out;
   const T* xr = x + (size_t)r_in * ldx;
@@ -1446,26 +1462,22 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const T* __restrict__ x, i
   const bool vec = sizeof(T) == 2 && D % 8 == 0 && ldx % 8 == 0;
   float ss = 0.f;
   if (vec) {
-    for (int i = threadIdx.x * V; i < D; i += 256 * V) {
+    for (int i = threadIdx.x * V; i < D; i += NORM_THREADS * V) {
       T v[V];
       *(uint4*)v = *(const uint4*)(xr + i);
 #pragma unroll
       for (int e = 0; e < V; ++e) ss += to_f(v[e]) * to_f(v[e]);
     }
   } else {
-    for (int i = threadIdx.x; i < D; i += 256) {
+    for (int i = threadIdx.x; i < D; i += NORM_THREADS) {
       const float v = to_f(xr[i]);
       ss += v * v;
     }
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
-  __syncthreads();
-  const float tot = red[0] + red[1] + red[2] + red[3];
+  const float tot = norm_block_sum(ss, red);
   const float inv = 1.0f / sqrtf(tot / (float)D + eps);
   if (vec) {
-    for (int i = threadIdx.x * V; i < D; i += 256 * V) {
+    for (int i = threadIdx.x * V; i < D; i += NORM_THREADS * V) {
       T v[V], gv[V], o[V];
       *(uint4*)v = *(const uint4*)(xr + i);
       *(uint4*)gv = *(const uint4*)(g + i);
@@ -1475,7 +1487,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const T* __restrict__ x, i
       *(uint4*)dst = *(const uint4*)o;
     }
   } else {
-    for (int i = threadIdx.x; i < D; i += 256) {
+    for (int i = threadIdx.x; i < D; i += NORM_THREADS) {
       const T o = from_f<T>(to_f(xr[i]) * inv * to_f(g[i]));
       y[ystride > 0 ? frag_off(r_out, i, ystride) : (size_t)r_out * ldy + i] = o;
     }
@@ -1486,10 +1498,10 @@ hipError_t launch_rmsnorm(int dtype, const void* x, int ldx, const int32_t* rows
                           long ystride, int n_rows, int D, float eps, hipStream_t s) {
   if (n_rows <= 0) return hipSuccess;
   if (dtype == AF_BF16)
-    hipLaunchKernelGGL(rmsnorm_kernel<bf16>, dim3(n_rows), dim3(256), 0, s, (const bf16*)x, ldx, rows,
+    hipLaunchKernelGGL(rmsnorm_kernel<bf16>, dim3(n_rows), dim3(NORM_THREADS), 0, s, (const bf16*)x, ldx, rows,
                        (const bf16*)g, (bf16*)y, ldy, ystride, D, eps);
   else
-    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(n_rows), dim3(256), 0, s, (const float*)x, ldx, rows,
+    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(n_rows), dim3(NORM_THREADS), 0, s, (const float*)x, ldx, rows,
                        (const float*)g, (float*)y, ldy, ystride, D, eps);
   return hipGetLastError();
 }
@@ -1499,10 +1511,10 @@ hipError_t launch_rmsnorm(int dtype, const void* x, int ldx, const int32_t* rows
 // would, so the residual row and the normalised row are bit-identical to that pair of launches
 // (one launch fewer, and the row is summed and normalised while it is on chip).
 template <typename T>
-__global__ __launch_bounds__(256) void resid_norm_kernel(const float* __restrict__ partial, int splits, T* x, int ldx,
+__global__ __launch_bounds__(NORM_THREADS) void resid_norm_kernel(const float* __restrict__ partial, int splits, T* x, int ldx,
                                                          const T* __restrict__ g, T* __restrict__ y, int ldy,
                                                          long ystride, int M, int D, float eps) {
-  __shared__ float red[4];
+  __shared__ float red[NORM_THREADS / 64];
   const int m = blockIdx.x;
   T* xr = x + (size_t)m * ldx;
   const size_t plane = (size_t)M * D;
@@ -1510,7 +1522,7 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(const float* __restrict
   const bool vec = sizeof(T) == 2 && D % 8 == 0 && ldx % 8 == 0;
   float ss = 0.f;
   if (vec) {
-    for (int i = threadIdx.x * V; i < D; i += 256 * V) {
+    for (int i = threadIdx.x * V; i < D; i += NORM_THREADS * V) {
       // all of this chunk's partial sums are requested before any is added (one memory latency
       // instead of one per split); they are added in split order
       constexpr int MAXS = 8;
@@ -1541,7 +1553,7 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(const float* __restrict
       for (int e = 0; e < 8; ++e) ss += to_f(r[e]) * to_f(r[e]);
     }
   } else {
-    for (int i = threadIdx.x; i < D; i += 256) {
+    for (int i = threadIdx.x; i < D; i += NORM_THREADS) {
       float v = 0.f;
       for (int sp = 0; sp < splits; ++sp) v += partial[sp * plane + (size_t)m * D + i];
       const T r = from_f<T>(to_f(xr[i]) + v);
@@ -1549,14 +1561,10 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(const float* __restrict
       ss += to_f(r) * to_f(r);
     }
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
-  __syncthreads();
-  const float tot = red[0] + red[1] + red[2] + red[3];
+  const float tot = norm_block_sum(ss, red);
   const float inv = 1.0f / sqrtf(tot / (float)D + eps);
   if (vec) {  // each thread re-reads only the elements it wrote
-    for (int i = threadIdx.x * V; i < D; i += 256 * V) {
+    for (int i = threadIdx.x * V; i < D; i += NORM_THREADS * V) {
       T v[V], gv[V], o[V];
       *(uint4*)v = *(const uint4*)(xr + i);
       *(uint4*)gv = *(const uint4*)(g + i);
@@ -1566,7 +1574,7 @@ __global__ __launch_bounds__(256) void resid_norm_kernel(const float* __restrict
       *(uint4*)dst = *(const uint4*)o;
     }
   } else {
-    for (int i = threadIdx.x; i < D; i += 256) {
+    for (int i = threadIdx.x; i < D; i += NORM_THREADS) {
       const T o = from_f<T>(to_f(xr[i]) * inv * to_f(g[i]));
       y[ystride > 0 ? frag_off(m, i, ystride) : (size_t)m * ldy + i] = o;
     }
@@ -1578,10 +1586,10 @@ hipError_t launch_resid_norm(int dtype, const float* partial, int splits, void* 
   if (M <= 0) return hipSuccess;
   if (splits < 1 || !partial) return hipErrorInvalidValue;
   if (dtype == AF_BF16)
-    hipLaunchKernelGGL(resid_norm_kernel<bf16>, dim3(M), dim3(256), 0, s, partial, splits, (bf16*)x, ldx,
+    hipLaunchKernelGGL(resid_norm_kernel<bf16>, dim3(M), dim3(NORM_THREADS), 0, s, partial, splits, (bf16*)x, ldx,
                        (const bf16*)g, (bf16*)y, ldy, ystride, M, D, eps);
   else
-    hipLaunchKernelGGL(resid_norm_kernel<float>, dim3(M), dim3(256), 0, s, partial, splits, (float*)x, ldx,
+    hipLaunchKernelGGL(resid_norm_kernel<float>, dim3(M), dim3(NORM_THREADS), 0, s, partial, splits, (float*)x, ldx,
                        (const float*)g, (float*)y, ldy, ystride, M, D, eps);
   return hipGetLastError();
 }
