@@ -735,9 +735,9 @@ __global__ __launch_bounds__(256, 1) void gemm32x2_kernel(GemmArgs a) {
 // Six-wave variant for 161..320 rows: the tile is 160 rows x 192 columns, each wave owning one
 // 32-column weight block over all five row blocks, so no weight fragment is loaded twice and
 // 2 x N / 192 workgroups (times the K split) fill the GPU where 288 x 128 tiles leave a quarter
-// of it idle.  Activations go through the LDS ring
-// by DMA issued by waves 0..3 (waves 4 and 5 issue none; every wave waits for its own loads and
-// then the barrier), the weights stream into per-wave register rings as in gemm32x2_kernel.
+// of it idle.  Activations go through the LDS ring by DMA issued by waves 0..3 (waves 4 and 5
+// issue none; every wave waits for its own loads and then the barrier), the weights stream into
+// per-wave register rings as in gemm32x2_kernel.
 // With a K split the kernel writes fp32 partial sums and splitk_reduce_kernel applies the
 // epilogue; unsplit it applies the epilogue itself.
 template <int FM, int NW, int EPI>
@@ -874,12 +874,12 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm32c_kernel(GemmArgs a) {
   }
 }
 
-// The six-wave tile is taken at 161..320 rows, unsplit or split two ways over K, when it fills
-// 3/4 of the GPU or more in one pass (a 7B-shape step's gate/up projection: 2 x 115 = 230
-// workgroups; its QKV projection: 2 x 64 x 2 = 256),
-// and for narrow projections (N <= 4224) split four ways for K <= 4096, five ways beyond (the
-// output and down projections: 2 x 22 x 4 = 176 and 2 x 22 x 5 = 220 workgroups), which write
-// about half the fp32 partial sums of the 8-way split the 288 x 128 tile needs to fill the GPU.
+// The six-wave tile is taken at 161..320 rows in two cases:
+//  * unsplit or split two ways over K, when it fills 3/4 of the GPU or more in one pass (a
+//    7B-shape step's gate/up projection: 2 x 115 = 230 workgroups; QKV: 2 x 64 x 2 = 256);
+//  * narrow projections (N <= 4224), split four ways for K <= 4096 and five ways beyond (the
+//    output and down projections: 2 x 22 x 4 = 176 and 2 x 22 x 5 = 220 workgroups), which
+//    write about half the fp32 partial sums of the 8-way split the 288 x 128 tile needs.
 constexpr int C6_FM = 5, C6_NW = 6;
 static int c6_narrow(int M, int N, int Kp) {
   const int mb = (M + 31) / 32, nb = (N + 31) / 32, units = Kp / 256;
