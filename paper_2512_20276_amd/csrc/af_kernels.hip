@@ -732,12 +732,12 @@ __global__ __launch_bounds__(256, 1) void gemm32x2_kernel(GemmArgs a) {
   }
 }
 
-// Six-wave variant for 161..320 rows: the tile is 160 rows x 192 columns, each wave owning one
+// NW-wave variant for 161..320 rows: the tile is 160 rows x 32 NW columns, each wave owning one
 // 32-column weight block over all five row blocks, so no weight fragment is loaded twice and
-// 2 x N / 192 workgroups (times the K split) fill the GPU where 288 x 128 tiles leave a quarter
-// of it idle.  Activations go through the LDS ring by DMA issued by waves 0..3 (waves 4 and 5
-// issue none; every wave waits for its own loads and then the barrier), the weights stream into
-// per-wave register rings as in gemm32x2_kernel.
+// two row tiles fill the GPU where 288 x 128 tiles leave part of it idle.  Activations go
+// through the LDS ring by DMA issued by waves 0..3 (any further waves issue none; every wave
+// waits for its own loads and then the barrier), the weights stream into per-wave register
+// rings as in gemm32x2_kernel.
 // With a K split the kernel writes fp32 partial sums and splitk_reduce_kernel applies the
 // epilogue; unsplit it applies the epilogue itself.
 template <int FM, int NW, int EPI>
@@ -874,17 +874,18 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm32c_kernel(GemmArgs a) {
   }
 }
 
-// The six-wave tile is taken at 161..320 rows in two cases:
-//  * unsplit or split two ways over K, when it fills 3/4 of the GPU or more in one pass (a
-//    7B-shape step's gate/up projection: 2 x 115 = 230 workgroups; QKV: 2 x 64 x 2 = 256);
-//  * narrow projections (N <= 4224), split four ways for K <= 4096 and five ways beyond (the
-//    output and down projections: 2 x 22 x 4 = 176 and 2 x 22 x 5 = 220 workgroups), which
-//    write about half the fp32 partial sums of the 8-way split the 288 x 128 tile needs.
+// The 160-row tiles are taken at 161..320 rows in two cases:
+//  * six waves (192 columns), unsplit or split two ways over K, when that fills 3/4 of the GPU
+//    or more in one pass (a 7B-shape step's gate/up projection: 2 x 115 = 230 workgroups; QKV:
+//    2 x 64 x 2 = 256);
+//  * four waves (128 columns) for narrow projections (N <= 4096) split four ways over K (the
+//    output and down projections: 2 x 32 x 4 = 256 workgroups), which write half the fp32
+//    partial sums of the 8-way split the 288 x 128 tile needs to fill the GPU.
 constexpr int C6_FM = 5, C6_NW = 6;
 static int c6_narrow(int M, int N, int Kp) {
   const int mb = (M + 31) / 32, nb = (N + 31) / 32, units = Kp / 256;
-  if (mb <= C6_FM || mb > 2 * C6_FM || nb > 132 || units < 4) return 0;
-  const int S = Kp <= 4096 ? 4 : 5, per = (units + S - 1) / S;
+  if (mb <= C6_FM || mb > 2 * C6_FM || nb > 128 || units < 4) return 0;
+  const int S = 4, per = (units + S - 1) / S;
   return (units + per - 1) / per;
 }
 static bool use_c6(const GemmArgs& a) {
@@ -896,6 +897,11 @@ static bool use_c6(const GemmArgs& a) {
 
 static hipError_t gemm32c_launch(int epi, const GemmArgs& a, hipStream_t s) {
   const int mb = (a.M + 31) / 32, nb = (a.N + 31) / 32;
+  if (a.splits > 1 && a.splits == c6_narrow(a.M, a.N, a.Kp)) {  // narrow: four-wave 160 x 128 tile
+    const dim3 grid(((mb + C6_FM - 1) / C6_FM) * ((nb + 3) / 4) * a.splits);
+    hipLaunchKernelGGL((gemm32c_kernel<C6_FM, 4, EPI_STORE>), grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
   const dim3 grid(((mb + C6_FM - 1) / C6_FM) * ((nb + C6_NW - 1) / C6_NW) * a.splits), block(64 * C6_NW);
   if (a.splits > 1) {  // partial sums only: one instance serves every epilogue
     hipLaunchKernelGGL((gemm32c_kernel<C6_FM, C6_NW, EPI_STORE>), grid, block, 0, s, a);
