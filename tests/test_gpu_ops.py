@@ -85,6 +85,22 @@ def test_linear_qkv_width_split_k(M):
     _assert_close(y, ref, "bf16", "linear", min_exact=0.99, atol=1e-3, rtol=8e-3)
 
 
+@pytest.mark.parametrize("M", [161, 282, 320])
+@pytest.mark.parametrize("K", [4096, 11008])
+def test_linear_narrow_split_k(M, K):
+    """N = 4096 (the output and down projections' width) at 161..320 rows: the four-wave
+    160 x 128 tile split four ways over K (K = 11008: splits of 11 and 10 k units), two row
+    tiles with a ragged second one; partial sums and reduce against fp64."""
+    N = 4096
+    x = wl.draw(("t_lin_x", M, K), (M, K), device="cuda")
+    w = wl.draw(("t_lin_w", N, K), (N, K), std=0.02, device="cuda")
+    y = torch.full((M, N), float("nan"), dtype=torch.bfloat16, device="cuda")
+    af.op_linear(x, w, y)
+    torch.cuda.synchronize()
+    ref = round_storage(linear(to_np(x), to_np(w)), "bf16")
+    _assert_close(y, ref, "bf16", "linear", min_exact=0.99, atol=1e-3, rtol=8e-3)
+
+
 def test_linear_large_m():
     """M = 2264 (eight 283-row pipelines), several M tiles and a ragged tail."""
     M, N, K = 2264, 512, 4096
