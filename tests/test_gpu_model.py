@@ -239,9 +239,10 @@ def test_7b_32_layer_pipeline_first_request_matches_definition():
 @pytest.mark.timeout(900)
 @pytest.mark.parametrize("split_k", [False, True])
 def test_7b_32_layer_packed_equals_sequential_on_gpu(split_k):
-    """The paper's losslessness claim on the GPU at full size: the packed pipeline (K = 7) and
-    the plain per-request run on the same kernels (a 276-row prefill alone, then single-row
-    decodes, each request in its own ring).  Every kernel computes a row independently of the
+    """The paper's losslessness claim on the GPU at full size: the packed pipeline (K = 7, 8
+    slots, run until the slots have wrapped) and the plain per-request run on the same kernels
+    (a 276-row prefill alone, then single-row decodes, each request in its own ring), for
+    requests 0, 1 and 9 (in a recycled slot).  Every kernel computes a row independently of the
     rows packed with it.  With split-K off (AF_OPT_NO_SPLIT_K) every row, logit and token is
     bit-identical.  With the default split-K the prefill rows still are (their GEMMs pick the
     same split factors in both runs); a decode row alone (M = 1) picks other factors, i.e.
@@ -266,13 +267,16 @@ def test_7b_32_layer_packed_equals_sequential_on_gpu(split_k):
 
     ring = af.Ring(shape.n_layers, 8, 288, shape.n_heads, shape.head_dim, dtype=torch.bfloat16)
     pipe = Pipeline(w, ring, K, pids, prefill_embeds, keep_logits=True)
-    rows, logits = {0: {}, 1: {}}, {0: {}, 1: {}}
-    for t in range(K + 1):
+    # requests 0 and 1, and request 9, which reuses request 1's slot once the ring has wrapped
+    rows, logits, slots = {0: {}, 1: {}, 9: {}}, {0: {}, 1: {}, 9: {}}, {}
+    for t in range(9 + K):
         res = pipe.step()
         for j, sg in enumerate(res.segments):
             if sg[4] in rows:
                 rows[sg[4]][sg[3]] = to_np(res.hidden[sg[0]:sg[0] + sg[1]])
                 logits[sg[4]][sg[3]] = to_np(res.logits[j])
+                slots[sg[4]] = sg[2]
+    assert slots[9] == slots[1]
     packed_tokens = {r: pipe.request_tokens(r) for r in rows}
     ring.close()
     D, V = shape.d_model, shape.vocab
