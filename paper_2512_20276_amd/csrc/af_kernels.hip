@@ -744,10 +744,14 @@ template <int FM, int NW, int EPI>
 __global__ __launch_bounds__(64 * NW, 1) void gemm32c_kernel(GemmArgs a) {
   constexpr int KS = 4, NBUF = 4, PFB = 8, BLK = 512;
   constexpr int SB = FM * KS;  // fragment blocks per stage
-  constexpr int DW = SB / 4;   // DMAs per stage of each of waves 0..3
+  // the activation DMAs: with six waves, waves 0 and 1 share SIMDs with waves 4 and 5, so the
+  // two waves alone on theirs (2 and 3) issue all of them; with four, every wave a quarter
+  constexpr int NDW = NW == 6 ? 2 : 4;  // waves issuing DMAs
+  constexpr int DW0 = NW == 6 ? 2 : 0;  // the first of them
+  constexpr int DW = SB / NDW;          // DMAs per stage of each
   constexpr int P = PFB / KS;  // stages of weight lookahead
   constexpr int TC = 32 * NW;  // tile columns
-  static_assert(NW >= 4 && SB % 4 == 0 && (NBUF * KS) % PFB == 0 && P >= 1, "pipeline shape");
+  static_assert((NW == 4 || NW == 6) && SB % NDW == 0 && (NBUF * KS) % PFB == 0 && P >= 1, "pipeline shape");
   constexpr int AS_BYTES = NBUF * SB * BLK * 2, T_BYTES = 32 * FM * TC * 4;
   __shared__ __attribute__((aligned(1024))) char smem[AS_BYTES > T_BYTES ? AS_BYTES : T_BYTES];
   bf16(*As)[SB * BLK] = (bf16(*)[SB * BLK])smem;
@@ -772,7 +776,7 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm32c_kernel(GemmArgs a) {
     constexpr int D = decltype(d_c)::value;  // DMAs per stage issued by this wave
     auto dma = [&](auto buf, int st) {
       static_for<0, D>([&](auto d) {
-        const int q = wave + 4 * decltype(d)::value, mb = q / KS, j = q % KS;
+        const int q = (wave - DW0) + NDW * decltype(d)::value, mb = q / KS, j = q % KS;
         const int k = min(kb + st * KS + j, ks16 - 1);
         const int blk = min(mt * FM + mb, m_blocks - 1);  // rows past M: a valid block, never stored
         const bf16* src = Ab + (size_t)blk * a.astride + (size_t)k * BLK + lane * 8;
@@ -844,7 +848,7 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm32c_kernel(GemmArgs a) {
       });
     });
   };
-  if (wave < 4)
+  if (wave >= DW0 && wave < DW0 + NDW)
     body(std::integral_constant<int, DW>{});
   else
     body(std::integral_constant<int, 0>{});
