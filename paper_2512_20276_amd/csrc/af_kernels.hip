@@ -735,9 +735,9 @@ __global__ __launch_bounds__(256, 1) void gemm32x2_kernel(GemmArgs a) {
 // NW-wave variant for 161..320 rows: the tile is 160 rows x 32 NW columns, each wave owning one
 // 32-column weight block over all five row blocks, so no weight fragment is loaded twice and
 // two row tiles fill the GPU where 288 x 128 tiles leave part of it idle.  Activations go
-// through the LDS ring by DMA issued by waves 0..3 (any further waves issue none; every wave
-// waits for its own loads and then the barrier), the weights stream into per-wave register
-// rings as in gemm32x2_kernel.
+// through the LDS ring by DMA (issued by some of the waves, see below; every wave waits for its
+// own loads and then the barrier), the weights stream into per-wave register rings as in
+// gemm32x2_kernel.
 // With a K split the kernel writes fp32 partial sums and splitk_reduce_kernel applies the
 // epilogue; unsplit it applies the epilogue itself.
 template <int FM, int NW, int EPI>
