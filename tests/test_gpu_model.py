@@ -312,3 +312,59 @@ def test_7b_32_layer_packed_equals_sequential_on_gpu(split_k):
             assert seq_tok == packed_tokens[r][1:]
         sring.close()
     w.close()
+
+
+@pytest.mark.timeout(600)
+def test_7b_k32_packed_equals_sequential_4_layers():
+    """The largest K of the K sweep (K = 32: a 276-row prefill packed with 31 decode rows, M =
+    307, whose decode rows take their own attention launch): with split-K off every row, logit
+    and token of requests 0 and 1 equals the plain per-request run on the same kernels, bit for
+    bit (a 4-layer model of the 7B shape)."""
+    shape = wl.LLAMA7B.with_layers(4)
+    K, L_V, L_T = 32, 256, 20
+    L_P, D, V = L_V + L_T, shape.d_model, shape.vocab
+    g, layers, w = _weights(shape)
+    del g, layers
+    w.set_options(af.AF_OPT_NO_SPLIT_K)
+    text = wl.draw_ids(("instruction", 0), L_T, V, device="cuda")
+    pids = torch.cat([torch.full((L_V,), -1, dtype=torch.int32, device="cuda"), text])
+    pool = {}
+
+    def prefill_embeds(t):
+        if t not in pool:
+            e = torch.zeros((L_P + K - 1, D), dtype=torch.bfloat16, device="cuda")
+            e[:L_V] = wl.draw(("vision", 0, t), (L_V, D), device="cuda")
+            pool[t] = e
+        return pool[t]
+
+    ring = af.Ring(shape.n_layers, K + 1, L_P + K, shape.n_heads, shape.head_dim, dtype=torch.bfloat16)
+    pipe = Pipeline(w, ring, K, pids, prefill_embeds, keep_logits=True)
+    rows, logits, Ms = {0: {}, 1: {}}, {0: {}, 1: {}}, []
+    for t in range(K + 1):
+        res = pipe.step()
+        Ms.append(res.M)
+        for j, sg in enumerate(res.segments):
+            if sg[4] in rows:
+                rows[sg[4]][sg[3]] = to_np(res.hidden[sg[0]:sg[0] + sg[1]])
+                logits[sg[4]][sg[3]] = to_np(res.logits[j])
+    assert max(Ms) == L_P + K - 1 == 307
+    packed_tokens = {r: pipe.request_tokens(r) for r in rows}
+    ring.close()
+    for r in rows:
+        sring = af.Ring(shape.n_layers, 1, L_P + K, shape.n_heads, shape.head_dim, dtype=torch.bfloat16)
+        hid = torch.empty((L_P, D), dtype=torch.bfloat16, device="cuda")
+        tok = torch.empty(1, dtype=torch.int32, device="cuda")
+        z = torch.empty((1, V), dtype=torch.float32, device="cuda")
+        s = sring.append(r, L_P)
+        af.packed_forward(w, pids.clone(), prefill_embeds(r)[:L_P], [(0, L_P, s.slot, 0, r, 1)], sring, hid, z, tok)
+        assert np.array_equal(to_np(hid), rows[r][0]), f"request {r}: prefill rows differ"
+        assert np.array_equal(to_np(z)[0], logits[r][0]) and int(tok.item()) == packed_tokens[r][0]
+        for j in range(1, K):
+            s = sring.append(r, 1)
+            feed = torch.tensor([packed_tokens[r][j - 1]], dtype=torch.int32, device="cuda")
+            h1 = torch.empty((1, D), dtype=torch.bfloat16, device="cuda")
+            af.packed_forward(w, feed, None, [(0, 1, s.slot, s.pos0, r, 1)], sring, h1, z, tok)
+            assert np.array_equal(to_np(h1), rows[r][s.pos0]), f"request {r}: decode {j} differs"
+            assert np.array_equal(to_np(z)[0], logits[r][s.pos0]) and int(tok.item()) == packed_tokens[r][j]
+        sring.close()
+    w.close()
