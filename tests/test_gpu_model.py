@@ -51,9 +51,15 @@ def check_tokens(gpu_tokens, oracle_logits, gpu_logits):
 
 
 # ----------------------------------------------------------------------------- tiny fp32 pipeline
-def test_tiny_fp32_pipeline_matches_oracle():
+@pytest.mark.parametrize("K", [3, 8])
+def test_tiny_fp32_pipeline_matches_oracle(K):
+    """K = 3 is the tiny configuration (step 2 packs 32 + 1 + 1 = 34 rows); K = 8 packs seven
+    decode rows beside each prefill (an odd number: the last pair of decode rows is half idle)
+    and wraps a 9-slot ring."""
     shape = wl.TINY
-    K, L_P, n_slots, max_pos = 3, 32, 4, 64
+    L_P = 32
+    n_slots, max_pos = (4, 64) if K == 3 else (K + 1, L_P + K)
+    n_steps = 7 if K == 3 else 2 * K + 2
     g, layers, w = _weights(shape, random_gains=True)
     ring = af.Ring(shape.n_layers, n_slots, max_pos, shape.n_heads, shape.head_dim, dtype=torch.float32)
     fn = tiny_prefill_fn(shape, L_P, seed=0)   # token ids uniform in [0, 512)
@@ -68,7 +74,7 @@ def test_tiny_fp32_pipeline_matches_oracle():
     opipe = PipelineOracle(model, K, n_slots, max_pos, fn)
     pipe = Pipeline(w, ring, K, torch.full((L_P,), -1, dtype=torch.int32, device="cuda"), prefill_embeds,
                     keep_logits=True)
-    for t in range(7):
+    for t in range(n_steps):
         ids_t, _ = fn(t)
         pipe.ids[t % 2][:L_P] = torch.from_numpy(ids_t).to(torch.int32).cuda()
         res = pipe.step()
@@ -81,7 +87,7 @@ def test_tiny_fp32_pipeline_matches_oracle():
         rep = allclose_report(to_np(res.logits), ost["logits"], atol=1e-4, rtol=1e-4)
         assert rep["ok"], (t, rep)
         check_tokens(got_tokens, ost["logits"], to_np(res.logits))
-        if t == 2:
+        if K == 3 and t == 2:
             assert res.M == 34
     # GPU ring == oracle ring for the live requests
     owners, lens, _ = ring.state()
