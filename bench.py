@@ -667,7 +667,7 @@ def main():
         at_ms, at_n = tm["attention"]
         at_bytes = attention_bytes(segs_seen, H, hd)
         at_gbs = at_bytes / (at_ms / at_n * 1e-3) / 1e9
-        out["roofline"] = {"kernel": "gemm_kernel, SwiGLU epilogue (gate/up projection)",
+        out["roofline"] = {"kernel": "gemm32c_kernel<5, 6, EPI_SWIGLU> (gate/up projection, SwiGLU epilogue)",
                            "bound": "hbm", "achieved": round(ga_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                            "frac": round(ga_gbs / PEAK_HBM_GBS, 4), "traffic": measured_traffic(),
                            "bytes_per_launch": ga_bytes, "avg_launch_us": round(ga_avg * 1e3, 2),
