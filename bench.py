@@ -36,6 +36,9 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+EXTRAS = ("sequential", "attention_stress", "sweep", "stress", "k_sweep", "copy_shift", "naive_pipe")
+
+
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
@@ -45,7 +48,9 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
     p.add_argument("--no-timing-pass", action="store_true")
     p.add_argument("--no-extra", action="store_true",
-                   help="skip the sequential-baseline and decode-heavy attention measurements")
+                   help="skip the measurements beside the packed step (baseline, attention, sweeps, ablations)")
+    p.add_argument("--extra", action="append", choices=EXTRAS, default=None,
+                   help="run only these measurements beside the packed step (repeatable; default: all)")
     p.add_argument("--copy-calibration", action="store_true",
                    help="before warm-up, run one streaming copy of COPY_BYTES (read once, written once) "
                         "whose hardware-counter readings scale the FETCH_SIZE / WRITE_SIZE of the others")
@@ -145,6 +150,26 @@ def summarize_pmc(fetch_csv, write_csv):
         wk = w.get(k, (0.0, 0))[0]
         tb = f[k][0] * 1024 * fs + wk * 1024 * ws
         print(f"| {k} | {f[k][1]} | {f[k][0]:.0f} | {wk:.0f} | {tb:.4g} |")
+    # attention launches by instance and grid (the decode-only instance at a given grid is one
+    # workload, e.g. the 56 decode rows x 32 heads of the stress mix)
+    def per_grid(path, counter):
+        acc = defaultdict(lambda: [0.0, 0])
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter or "attention_kernel" not in r["Kernel_Name"]:
+                continue
+            inst = "decode-only" if "Lb0E" in r["Kernel_Name"] else "query tiles + decode rows"
+            a = acc[(inst, int(r["Grid_Size"]), int(r["Workgroup_Size"]))]
+            a[0] += float(r["Counter_Value"])
+            a[1] += 1
+        return {k: (v / n, n) for k, (v, n) in acc.items()}
+    fa, wa = per_grid(fetch_csv, "FETCH_SIZE"), per_grid(write_csv, "WRITE_SIZE")
+    if fa:
+        print("\n| attention instance | workgroups | dispatches | FETCH KiB | WRITE KiB | HBM bytes (scaled) |")
+        print("|---|---:|---:|---:|---:|---:|")
+        for k in sorted(fa, key=lambda k: -fa[k][0]):
+            wk = wa.get(k, (0.0, 0))[0]
+            print(f"| {k[0]} | {k[1] // k[2]} | {fa[k][1]} | {fa[k][0]:.0f} | {wk:.0f} | "
+                  f"{fa[k][0] * 1024 * fs + wk * 1024 * ws:.4g} |")
     g = "gemm (gate/up + SwiGLU)"
     if g in f:
         tb = int(round(f[g][0] * 1024 * fs + w[g][0] * 1024 * ws))
@@ -681,7 +706,8 @@ def main():
         out["timing_pass_ms_per_step"] = round(t_inst / args.steps * 1e3, 4)
         log(f"timing pass: {json.dumps(per_step)}")
 
-    if not args.no_extra:
+    extras = () if args.no_extra else tuple(args.extra or EXTRAS)
+    if "sequential" in extras:
         log("sequential baseline (one request at a time, same kernels)")
         seq_ms = sequential_baseline(af, w, shape, pids, pool, K)
         out["sequential_baseline"] = {
@@ -689,16 +715,22 @@ def main():
             "packed_speedup": round(steps_s / (1e3 / seq_ms), 3),
             "note": "one request = 276-row prefill + 6 single-row decodes through 32 layers; the packed "
                     "pipeline completes one request per step"}
+    if "attention_stress" in extras:
         log("decode-heavy attention (8 pipelines x (276 + 7), 64 slots)")
         out["attention_stress"] = decode_heavy_attention(af, w, shape)
+    if "sweep" in extras:
         log("packed-mix sweep (one layer, 16 points)")
         out["sweep"] = sweep(af, w, shape)
+    if "stress" in extras:
         log("stress workload (8 pipelines, M = 2264, 32 layers)")
         out["stress"] = stress(af, w, shape)
+    if "k_sweep" in extras:
         log("K sweep (K = 7, 16, 24, 32)")
         out["k_sweep"] = k_sweep(af, w, shape, pids)
+    if "copy_shift" in extras:
         log("physical-copy stage shift (the paper's InPlaceKVShift copy) against the rotation")
         out["copy_shift"] = copy_shift(af, w, shape, pids, pool, K)
+    if "naive_pipe" in extras:
         log("naive pipe (per-request caches, per-layer gather/scatter, host-coordinated)")
         out["naive_pipe"] = naive_pipe(af, w, shape, pids, pool, ms_step, K)
     ring.close()
