@@ -174,6 +174,7 @@ class OracleModel:
         values of every row into its request's ring slot.  Returns the updated state."""
         lw, H, hd, eps = self.layers[l], self.H, self.hd, self.shape.rms_eps
         M = x.shape[0]
+        x_in = x
         pos = np.empty(M, dtype=np.int64)
         for sg in segs:
             pos[sg.q_start:sg.q_start + sg.q_len] = sg.pos0 + np.arange(sg.q_len)
@@ -201,11 +202,12 @@ class OracleModel:
         # (InPlaceShiftKV moves no data here: slots are recycled by the bookkeeping.)
         # OutputProj + residual, then the MLP residual (standard Llama block)
         x = self.rs(x + linear(o, lw["wo"]))
+        x_mid = x
         m = self.rs(rmsnorm(x, lw["mlp_norm"], eps))
         a = self.rs(silu(linear(m, lw["w_gate"])) * linear(m, lw["w_up"]))
         x = self.rs(x + linear(a, lw["w_down"]))
         if trace is not None:
-            trace.append(dict(n=n, q=q, k=k, v=v, o=o, a=a, x=x))
+            trace.append(dict(x_in=x_in, n=n, q=q, k=k, v=v, o=o, x_mid=x_mid, a=a, x=x))
         return x
 
     # ------------------------------------------------------------------ head

@@ -122,9 +122,10 @@ class PipelineOracle:
         its L_P rows), then the decode row of request t-s for s = 1..K-1 (those that exist)."""
         return [(t - s, -1 if s == 0 else 1) for s in range(self.K) if t - s >= 0]
 
-    def step(self, forced: Optional[Sequence[int]] = None):
+    def step(self, forced: Optional[Sequence[int]] = None, trace: Optional[list] = None):
         """Run one packed step.  Returns dict(t, segments, ids, embeds, hidden, logits,
-        tokens (oracle argmax), used (tokens fed back), margins, done {request: K tokens})."""
+        tokens (oracle argmax), used (tokens fed back), margins, done {request: K tokens}).
+        With ``trace`` (a list), each layer appends its input, intermediates and output."""
         t, K, D = self.t, self.K, self.model.shape.d_model
         ids_rows, emb_rows, segs = [], [], []
         row = 0
@@ -144,7 +145,7 @@ class PipelineOracle:
             row += n
         ids = np.concatenate(ids_rows)
         embeds = np.concatenate(emb_rows)
-        hidden, z, toks = self.model.forward_packed(ids, embeds, segs, self.kv)
+        hidden, z, toks = self.model.forward_packed(ids, embeds, segs, self.kv, trace)
         used = list(toks) if forced is None else [int(v) for v in forced]
         done = {}
         for sg, tok in zip(segs, used):

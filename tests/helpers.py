@@ -87,7 +87,8 @@ def gpu_shape_weights(shape, seed=0, random_gains=False):
     return wl.model_weights(shape, seed=seed, device="cuda", random_gains=random_gains)
 
 
-def bf16_layer_parity(got, ref, atol=2e-2, rtol=1e-2, outlier_frac=1e-4, norm_rel=1e-2):
+def bf16_layer_parity(got, ref, atol=2e-2, rtol=1e-2, outlier_frac=1e-4, norm_rel=1e-2, row_norm_rel=1e-2,
+                      outlier_cap=3.0):
     """Parity of bf16 hidden states that went through a whole layer (or more).
 
     Every stored intermediate is rounded to bf16 on both sides, so an fp32-vs-float64
@@ -95,18 +96,57 @@ def bf16_layer_parity(got, ref, atol=2e-2, rtol=1e-2, outlier_frac=1e-4, norm_re
     ulp, and later layers mix such flips into many elements.  Measured on one 7B layer: the
     attention output is 98.9% bit-identical, the residual after the MLP 57%.  Where the
     residual update cancels a large input, a one-ulp flip of the large term remains as an
-    absolute error on a small result.  The bound therefore has two parts:
-      normwise   ||got - ref||_2 <= norm_rel * ||ref||_2                 (rel 1e-2)
+    absolute error on a small result.  The bound therefore has four parts:
+      normwise    ||got - ref||_2 <= norm_rel ||ref||_2 over the whole tensor        (1e-2)
+      per row     ||got_r - ref_r||_2 <= row_norm_rel ||ref_r||_2 for every row      (1e-2)
       elementwise |got - ref| <= atol + rtol |ref| for all but outlier_frac of the elements
-                                                                       (max-abs 2e-2 / rel 1e-2)
-    Single steps on identical inputs are held to the elementwise bound with no outliers."""
+                                                           (max-abs 2e-2 / rel 1e-2; 1e-4)
+      outliers    no element beyond outlier_cap times its elementwise bound          (3x)
+    Measured on single 7B layers (M = 1 .. 2264, and each of the 32 layers of a 32-layer step
+    from the oracle's input): normwise <= 0.0028, per row <= 0.0047, at most 8.1e-5 of the
+    elements outside the elementwise bound, none beyond 2.4x.
+    The last axis is the row; a 1-d input is one row.  Single steps on identical inputs are
+    held to the elementwise bound with no outliers."""
     rep = allclose_report(got, ref, atol, rtol)
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
-    rep["norm_rel"] = float(np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30))
+    diff = got - ref
+    rep["norm_rel"] = float(np.linalg.norm(diff) / max(np.linalg.norm(ref), 1e-30))
     rep["outlier_frac"] = rep["n_bad"] / max(ref.size, 1)
-    rep["ok"] = rep["norm_rel"] <= norm_rel and rep["outlier_frac"] <= outlier_frac
+    d2 = np.atleast_2d(diff).reshape(-1, ref.shape[-1] if ref.ndim else 1)
+    r2 = np.atleast_2d(ref).reshape(d2.shape)
+    row_rel = np.linalg.norm(d2, axis=1) / np.maximum(np.linalg.norm(r2, axis=1), 1e-30)
+    row_rel = np.where(np.isfinite(row_rel), row_rel, np.inf)
+    rep["row_norm_rel"] = float(row_rel.max(initial=0.0))
+    ratio = np.abs(diff) / (atol + rtol * np.abs(ref))
+    ratio = np.where(np.isfinite(ratio), ratio, np.inf)
+    rep["worst_ratio"] = float(ratio.max(initial=0.0))
+    rep["ok"] = (rep["norm_rel"] <= norm_rel and rep["outlier_frac"] <= outlier_frac
+                 and rep["row_norm_rel"] <= row_norm_rel and rep["worst_ratio"] <= outlier_cap)
     return rep
+
+
+def near_tie_window(dev, cap=0.05):
+    """Half-width of the near-tie window of a greedy token: twice the largest logit deviation
+    of its row, capped at ``cap`` (0.05), so a drift never excuses a clear margin."""
+    return np.minimum(2.0 * np.asarray(dev, dtype=np.float64), cap)
+
+
+def check_tokens(gpu_tokens, oracle_logits, gpu_logits, cap=0.05):
+    """Exact token equality wherever the oracle's top-2 margin exceeds the near-tie window;
+    returns the number of tokens inside the window (near-ties)."""
+    from oracle.pipeline import top2_margin
+    z = np.asarray(oracle_logits, dtype=np.float64)
+    margins = top2_margin(z)
+    dev = np.abs(np.asarray(gpu_logits, dtype=np.float64) - z).max(axis=1)
+    window = near_tie_window(dev, cap)
+    ties = 0
+    for i, tok in enumerate(gpu_tokens):
+        if margins[i] > window[i]:
+            assert int(tok) == int(np.argmax(z[i])), (i, int(tok), int(np.argmax(z[i])), margins[i], dev[i])
+        else:
+            ties += 1
+    return ties
 
 
 def exact_fraction(got, ref):

@@ -5,10 +5,12 @@
   states and logits to fp32 tolerance, tokens exactly.
 * One 7B-shape layer in bf16 on a pre-filled ring whose slots wrap: 276 prefill rows + 6
   decode rows at contexts 277..282 (M = 282); hidden to max-abs 2e-2 / rel 1e-2, ring cells.
-* 32-layer 7B-shape pipeline, K = 7: request 0's seven tokens and logits against the plain
-  per-request definition (sequential prefill + decodes), forced with the GPU's tokens.
+* 32-layer 7B-shape pipeline, K = 7, steps 0..6 against the oracle pipeline forced with the
+  GPU's tokens: each layer of the first full step (M = 282) run from the oracle's input and
+  ring history and held elementwise to 2e-2 + 1e-2 |ref|; error growth per layer; every
+  step's hidden rows, logits and tokens.
 Greedy tokens are compared exactly wherever the oracle's top-2 margin exceeds twice the
-largest logit deviation of that row; rows inside that window are near-ties.
+largest logit deviation of that row, capped at 0.05; rows inside that window are near-ties.
 """
 import math
 
@@ -18,9 +20,9 @@ import torch
 
 import oracle
 import workload as wl
-from oracle.pipeline import PipelineOracle, sequential_generate, top2_margin
-from tests.helpers import (advance_head, allclose_report, bf16_layer_parity, oracle_model, oracle_segments,
-                           reserve_step, tiny_prefill_fn, to_np)
+from oracle.pipeline import PipelineOracle
+from tests.helpers import (advance_head, allclose_report, bf16_layer_parity, check_tokens, oracle_model,
+                           oracle_segments, reserve_step, tiny_prefill_fn, to_np)
 
 pytestmark = pytest.mark.gpu
 af = pytest.importorskip("paper_2512_20276_amd")
@@ -33,21 +35,6 @@ HID_TOL_F32 = dict(atol=1e-4, rtol=1e-4)
 def _weights(shape, device="cuda", random_gains=False):
     g, layers = wl.model_weights(shape, seed=0, device=device, random_gains=random_gains)
     return g, layers, af.Weights(shape, g, layers)
-
-
-def check_tokens(gpu_tokens, oracle_logits, gpu_logits):
-    """Exact token equality outside the near-tie window; returns the number of near-ties."""
-    z = np.asarray(oracle_logits)
-    margins = top2_margin(z)
-    dev = np.abs(np.asarray(gpu_logits) - z).max(axis=1)
-    ties = 0
-    for i, tok in enumerate(gpu_tokens):
-        window = 2 * dev[i]
-        if margins[i] > window:
-            assert int(tok) == int(np.argmax(z[i])), (i, tok, int(np.argmax(z[i])), margins[i], dev[i])
-        else:
-            ties += 1
-    return ties
 
 
 # ----------------------------------------------------------------------------- tiny fp32 pipeline
@@ -193,13 +180,56 @@ def test_7b_layer_segment_order_and_slot_invariance():
 
 
 # ----------------------------------------------------------------------------- 32 layers
-@pytest.mark.timeout(600)
-def test_7b_32_layer_pipeline_first_request_matches_definition():
+def _layer_report(got, ref, tr=None):
+    """Layer-gate report; with the oracle's trace of the layer, also the number of elements
+    outside 2e-2 + 1e-2 x the residual stream's magnitude at that element (the largest of the
+    layer's input, its state after the attention residual and its output: the scale at which
+    the two residual adds round)."""
+    rep = bf16_layer_parity(got, ref)
+    out = {k: rep[k] for k in ("ok", "max_abs", "max_rel", "rms", "norm_rel", "row_norm_rel", "n_bad", "worst_ratio")}
+    if tr is not None:
+        scale = np.maximum(np.maximum(np.abs(ref), np.abs(tr["x_in"])), np.abs(tr["x_mid"]))
+        out["n_bad_stream_scale"] = int(np.sum(~(np.abs(np.asarray(got) - ref) <= 2e-2 + 1e-2 * scale)))
+    return out
+
+
+def _logits_report(got, ref):
+    rep = allclose_report(got, ref, atol=2e-2, rtol=1e-2)
+    rep["norm_rel"] = float(np.linalg.norm(np.asarray(got) - ref) / np.linalg.norm(ref))
+    return rep
+
+
+@pytest.mark.timeout(1200)
+def test_7b_32_layer_pipeline_matches_oracle(monkeypatch):
+    """The benchmark workload (32 layers, K = 7, 8 slots) against the oracle pipeline.
+
+    The GPU pipeline runs steps 0..6 on its own greedy tokens; the oracle pipeline (Alg. 1 over
+    the float64 packed forward with bf16 storage) runs the same steps forced with the GPU's
+    tokens, so the two trajectories never part.  Step 6 is the first full step: a 276-row
+    prefill and six decode rows at contexts 277..282 (M = 282).
+      * Per layer (the gate): each of the 32 layers of step 6 runs on the GPU from the
+        oracle's input to that layer, with the oracle's ring history of that layer, and is held
+        to the layer gate (max-abs 2e-2 / rel 1e-2 elementwise, normwise and per row).
+      * Head: the final norm, LM head and argmax run on the oracle's last hidden rows of every
+        step, and the last layer plus the head on the oracle's input to the last layer at step
+        6: logits elementwise to 2e-2 + 1e-2 |ref|; greedy tokens equal wherever the oracle's
+        top-2 margin exceeds min(2 x the row's largest logit deviation, 0.05) (near-ties inside
+        that window are counted and bounded).
+      * Growth: the 32 layers of step 6 chained on the GPU's own outputs from the oracle's
+        layer-0 input (error growth per layer inside one step), reported.
+      * End to end: every step's hidden rows and logits of the free-running pipeline.  Both
+        sides store bf16 after every layer, and a summation order that differs (fp32 MFMA against
+        float64) flips roundings that later layers mix into every element, so 32 layers drift.
+        The drift allowed is set by a second implementation of the same definition: the oracle
+        with its matrix products accumulated in float32 instead of float64, run over the same
+        32 layers of step 6.  The GPU's hidden rows and logits may drift from the float64 oracle
+        at most twice as far (normwise) as that float32 oracle does; tokens must agree outside
+        twice the observed logit deviation, and the capped-window count is reported.
+    """
     shape = wl.LLAMA7B
     K, L_V, L_T, n_slots, max_pos = 7, 256, 20, 8, 288
-    L_P = L_V + L_T
+    L_P, H, hd, V = L_V + L_T, shape.n_heads, shape.head_dim, shape.vocab
     g, layers, w = _weights(shape)
-    ring = af.Ring(shape.n_layers, n_slots, max_pos, shape.n_heads, shape.head_dim, dtype=torch.bfloat16)
     text = wl.draw_ids(("instruction", 0), L_T, shape.vocab, device="cuda")
     pids = torch.cat([torch.full((L_V,), -1, dtype=torch.int32, device="cuda"), text])
     pool = {}
@@ -211,35 +241,127 @@ def test_7b_32_layer_pipeline_first_request_matches_definition():
             pool[t] = e
         return pool[t]
 
+    ring = af.Ring(shape.n_layers, n_slots, max_pos, H, hd, dtype=torch.bfloat16)
     pipe = Pipeline(w, ring, K, pids, prefill_embeds, keep_logits=True)
-    logits0 = []
+    gpu = []
     for t in range(K):
         res = pipe.step()
-        logits0.append(to_np(res.logits[t]))   # request 0 is segment t at step t
-    torch.cuda.synchronize()
-    toks = pipe.request_tokens(0)
-    assert len(toks) == K
-    emb0 = to_np(prefill_embeds(0)[:L_P])
-    ids0 = pids.cpu().numpy().astype(np.int64)
-    del pool
-    w.close()
+        gpu.append(dict(segments=res.segments, hidden=to_np(res.hidden), logits=to_np(res.logits),
+                        tokens=res.tokens.cpu().tolist()))
     ring.close()
+    assert gpu[-1]["hidden"].shape[0] == 282
+    emb = {t: to_np(prefill_embeds(t)[:L_P]) for t in range(K)}
+    ids = pids.cpu().numpy().astype(np.int64)
+    del pool
     gh = {k: to_np(v) for k, v in g.items()}
     lh = [{k: to_np(v) for k, v in lw.items()} for lw in layers]
     del g, layers
     torch.cuda.empty_cache()
     model = oracle.OracleModel(shape, gh, lh, storage="bf16")
     del gh, lh
-    seq = sequential_generate(model, ids0, emb0, K, forced=toks)
-    z_gpu = np.stack(logits0)
-    rep = allclose_report(z_gpu, seq["logits"], atol=5e-2, rtol=2e-2)
-    rep["norm_rel"] = float(np.linalg.norm(z_gpu - seq["logits"]) / np.linalg.norm(seq["logits"]))
-    print("32-layer logits vs the per-request definition (free-running drift)", rep)
-    # 32 layers of bf16 storage compound the rounding-flip cascade of each layer; the logits
-    # are bounded normwise and the tokens must agree outside the near-tie window
-    assert rep["norm_rel"] < 0.1, rep
-    ties = check_tokens(toks, seq["logits"], z_gpu)
-    print("near-ties", ties, "tokens", toks, seq["tokens"])
+    opipe = PipelineOracle(model, K, n_slots, max_pos, lambda t: (ids, emb[t]))
+
+    def gpu_head(hidden_np, segs):
+        """Final norm + LM head + argmax of the GPU on the given bf16 rows."""
+        hid = torch.from_numpy(hidden_np).to(torch.bfloat16).cuda()
+        assert np.array_equal(to_np(hid), hidden_np)
+        z = torch.empty((len(segs), V), dtype=torch.float32, device="cuda")
+        tok = torch.empty(len(segs), dtype=torch.int32, device="cuda")
+        af.op_lm_head_argmax(w, hid, segs, z, tok)
+        return to_np(z), tok.cpu().tolist()
+
+    # ---- end to end, every step; the head on the oracle's hidden rows
+    trace, e2e, head = [], [], []
+    ties_head = n_head = capped_flips = 0
+    for t in range(K):
+        ost = opipe.step(forced=gpu[t]["tokens"], trace=trace if t == K - 1 else None)
+        assert gpu[t]["segments"] == [(s.q_start, s.q_len, s.slot, s.pos0, s.request_id, 1)
+                                      for s in ost["segments"]], t
+        hrep = _layer_report(gpu[t]["hidden"], ost["hidden"])
+        zrep = _logits_report(gpu[t]["logits"], ost["logits"])
+        # free-running tokens: exact outside twice the observed deviation
+        check_tokens(gpu[t]["tokens"], ost["logits"], gpu[t]["logits"], cap=np.inf)
+        try:
+            check_tokens(gpu[t]["tokens"], ost["logits"], gpu[t]["logits"])
+        except AssertionError:
+            capped_flips += 1
+        e2e.append(dict(t=t, hidden=hrep, logits={k: zrep[k] for k in ("max_abs", "rms", "norm_rel", "n_bad")},
+                        oracle_tokens=ost["tokens"], gpu_tokens=gpu[t]["tokens"]))
+        print("end-to-end step", t, e2e[-1], flush=True)
+        z, tok = gpu_head(ost["hidden"], gpu[t]["segments"])
+        hz = _logits_report(z, ost["logits"])
+        ties_head += check_tokens(tok, ost["logits"], z)
+        n_head += len(tok)
+        head.append(dict(t=t, ok=hz["ok"], max_abs=hz["max_abs"], rms=hz["rms"], n_bad=hz["n_bad"]))
+        print("head on the oracle's hidden, step", t, head[-1], flush=True)
+    print("head near-ties", ties_head, "of", n_head, "; free-running steps with a flip outside the capped window",
+          capped_flips, flush=True)
+    assert len(trace) == shape.n_layers
+
+    # ---- per layer, from the oracle's input and ring history (step 6)
+    segs6 = gpu[K - 1]["segments"]
+    lring = af.Ring(shape.n_layers, n_slots, max_pos, H, hd, dtype=torch.bfloat16)
+    for sg in sorted(segs6, key=lambda s: s[4]):      # request r holds slot r, as in the pipeline
+        if sg[3] > 0:
+            lring.append(sg[4], sg[3])
+    segs = reserve_step(lring, [(sg[4], sg[3], sg[1]) for sg in segs6])
+    assert [s[:4] for s in segs] == [s[:4] for s in segs6]
+    per_layer, growth = [], []
+    for l in range(shape.n_layers):
+        for sg in segs:
+            if sg[3] > 0:
+                kk = torch.from_numpy(opipe.kv.k[l, sg[2], :sg[3]]).to(torch.bfloat16).cuda()
+                vv = torch.from_numpy(opipe.kv.v[l, sg[2], :sg[3]]).to(torch.bfloat16).cuda()
+                lring.write_kv(l, sg[2], 0, kk, vv)
+        x = torch.from_numpy(trace[l]["x_in"]).to(torch.bfloat16).cuda()
+        assert np.array_equal(to_np(x), trace[l]["x_in"])
+        af.packed_layer_forward(w, l, x, segs, lring)
+        xl = to_np(x)
+        per_layer.append(_layer_report(xl, trace[l]["x"], trace[l]))
+        print("layer", l, "from the oracle's input", per_layer[-1], flush=True)
+    # last layer + head from the oracle's input to the last layer
+    z, tok = gpu_head(xl, segs6)
+    ost_z = opipe.model.logits(trace[-1]["x"][[s[0] + s[1] - 1 for s in segs6]])
+    last = _logits_report(z, ost_z)
+    ties_last = check_tokens(tok, ost_z, z)
+    print("last layer + head from the oracle's input", {k: last[k] for k in ("ok", "max_abs", "rms", "n_bad")},
+          "near-ties", ties_last, flush=True)
+    x = torch.from_numpy(trace[0]["x_in"]).to(torch.bfloat16).cuda()
+    for l in range(shape.n_layers):
+        af.packed_layer_forward(w, l, x, segs, lring)
+        growth.append(_layer_report(to_np(x), trace[l]["x"]))
+        print("layer", l, "chained on the GPU", growth[-1], flush=True)
+    lring.close()
+    w.close()
+
+    # the drift of a float32-accumulating oracle over the same step (same input and history)
+    import oracle.model as om
+
+    def linear_f32(x, wt):
+        return (np.asarray(x, np.float32) @ np.asarray(wt, np.float32).T).astype(np.float64)
+
+    monkeypatch.setattr(om, "linear", linear_f32)
+    osegs = oracle_segments(segs6)
+    x = trace[0]["x_in"]
+    floor = []
+    for l in range(shape.n_layers):
+        x = opipe.model.layer_packed(l, x, osegs, opipe.kv)
+        floor.append(_layer_report(x, trace[l]["x"]))
+        print("layer", l, "float32-accumulating oracle", floor[-1], flush=True)
+    z32 = opipe.model.logits(x[[s[0] + s[1] - 1 for s in segs6]])
+    monkeypatch.undo()
+    floor_z = _logits_report(z32, ost_z)
+    print("float32-accumulating oracle logits", {k: floor_z[k] for k in ("max_abs", "rms", "norm_rel", "n_bad")},
+          flush=True)
+
+    bad = [(l, r) for l, r in enumerate(per_layer) if not r["ok"]]
+    assert not bad, bad
+    assert last["ok"], last
+    assert all(h["ok"] for h in head), head
+    assert ties_head + ties_last <= 2, (ties_head, ties_last)
+    h_floor, z_floor = floor[-1]["norm_rel"], floor_z["norm_rel"]
+    for r in e2e:
+        assert r["hidden"]["norm_rel"] <= 2 * h_floor and r["logits"]["norm_rel"] <= 2 * z_floor, (r, h_floor, z_floor)
 
 
 @pytest.mark.timeout(900)
@@ -304,7 +426,8 @@ def test_7b_32_layer_packed_equals_sequential_on_gpu(split_k):
             h1 = torch.empty((1, D), dtype=torch.bfloat16, device="cuda")
             af.packed_forward(w, feed, None, [(0, 1, s.slot, s.pos0, r, 1)], sring, h1, z, tok)
             if split_k:
-                rep = bf16_layer_parity(to_np(h1), rows[r][s.pos0], norm_rel=0.1, outlier_frac=1.0)
+                rep = bf16_layer_parity(to_np(h1), rows[r][s.pos0], norm_rel=0.1, row_norm_rel=0.1,
+                                        outlier_frac=1.0, outlier_cap=np.inf)
                 assert rep["ok"], (r, j, rep)
             else:
                 assert np.array_equal(to_np(h1), rows[r][s.pos0]), f"request {r}: decode {j} differs"
@@ -313,7 +436,9 @@ def test_7b_32_layer_packed_equals_sequential_on_gpu(split_k):
             pk_z.append(logits[r][s.pos0])
             seq_tok.append(int(tok.item()))
         if split_k:
-            check_tokens(packed_tokens[r][1:], np.stack(pk_z), np.stack(seq_z))
+            # GPU against GPU with another fp32 summation order: the window is twice the
+            # observed deviation, not capped (the capped window is for oracle comparisons)
+            check_tokens(packed_tokens[r][1:], np.stack(pk_z), np.stack(seq_z), cap=np.inf)
         else:
             assert seq_tok == packed_tokens[r][1:]
         sring.close()

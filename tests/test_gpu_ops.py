@@ -134,14 +134,23 @@ ATTN_CASES = {
     "mixed_7b_step": [(10, 0, 276)] + [(10 - s, 276 + s - 1, 1) for s in range(1, 7)],
     "chunked_prefill": [(1, 100, 70), (2, 0, 1), (3, 5, 64), (4, 200, 1)],
     "single_key": [(1, 0, 1)],
+    # more than 16 decode rows beside a prefill at 32 heads: the query tiles and the decode
+    # rows take two launches (the K = 32 step of the K sweep, and the stress step's mix)
+    "k32_step": [(40, 0, 276)] + [(40 - s, 276 + s - 1, 1) for s in range(1, 32)],
+    "stress_mix": [(1000 + p, 0, 276) for p in range(8)] +
+                  [(1000 + 8 * s + p, 276 + s - 1, 1) for s in range(1, 8) for p in range(8)],
 }
+# cases that need a larger ring than 8 slots x 288, and run only at 32 heads x 128
+ATTN_RING = {"k32_step": (33, 320), "stress_mix": (64, 288)}
 
 
 @pytest.mark.parametrize("storage,H,hd", [("bf16", 32, 128), ("bf16", 4, 64), ("f32", 4, 64), ("f32", 2, 128)])
 @pytest.mark.parametrize("case", sorted(ATTN_CASES))
 def test_attention(storage, H, hd, case):
     dt = DT[storage]
-    n_slots, max_pos = 8, 288
+    n_slots, max_pos = ATTN_RING.get(case, (8, 288))
+    if case in ATTN_RING and (storage, H, hd) != ("bf16", 32, 128):
+        pytest.skip("two-launch cases run at the 7B head shape")
     ring = af.Ring(1, n_slots, max_pos, H, hd, dtype=dt)
     advance_head(ring, 3)  # start the rotation mid-ring so slots wrap
     K, V = _fill_ring(ring, 0, n_slots, max_pos, H, hd, dt, ("t_attn", storage, H, hd))
