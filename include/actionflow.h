@@ -18,6 +18,10 @@
  *  - Element type of weights, activations and the ring: af_dtype (bf16 or fp32);
  *    accumulation is always fp32.
  *  - Handles are not thread-safe; one handle must not be used by two threads at once.
+ *  - A weights object keeps one device copy of the step tables and one set of scratch
+ *    activations, and a ring one set of device KV: use each weights object and each ring on
+ *    a single stream (or order the streams yourself), since two calls in flight on different
+ *    streams would overwrite each other's tables and activations.
  *  - Ownership: the ring and the weights object own the device memory they allocate;
  *    caller buffers are only borrowed for the duration of a call.
  */
@@ -203,6 +207,31 @@ af_status af_weights_set_options(af_weights* w, uint32_t flags);
 
 /* Copies and clears the device error counter (ids out of range) after synchronizing hip_stream. */
 af_status af_weights_device_errors(af_weights* w, void* hip_stream, int32_t* count);
+
+/* ------------------------------------------------------------------ forward without allocation
+ * For callers that cannot allocate device memory during a step: code under HIP graph capture,
+ * serving loops and harnesses that forbid hipMalloc.  Not a step of the paper's method.
+ *
+ * af_packed_forward_noalloc takes the arguments of af_packed_forward, follows the same rules and
+ * returns the same results (bit for bit: the same kernels in the same order).  Every device
+ * workspace of the step (normalized rows, queries, attention output, the MLP activation, split-K
+ * partial sums, the step tables and the rotary table) is carved from one array of
+ * AF_NOALLOC_SCRATCH_BYTES (64 MiB) that the library holds on each GPU it runs on, from the
+ * first call there until the process ends.  The call allocates nothing: no hipMalloc, hipFree
+ * or pinned host memory (the step tables are copied from pageable host memory with
+ * hipMemcpyAsync on hip_stream).  The first call on a device looks up the array's address
+ * there, so that device must be current, as for every call.
+ *  - A step whose workspace would not fit (it grows with M, d_model, d_ff, the ring's max_pos
+ *    and the number of emitting rows; the 7B-shape step of 282 packed rows needs about 42 MiB)
+ *    is rejected with AF_ERR_OUT_OF_RANGE before any launch, the need and the limit in
+ *    af_last_error().
+ *  - Every call on one GPU shares that GPU's array, which keeps the last call's contents: calls
+ *    that overlap on one GPU (two streams, two threads) race and corrupt each other's results;
+ *    serialize them. */
+#define AF_NOALLOC_SCRATCH_BYTES (64ull * 1024 * 1024)
+af_status af_packed_forward_noalloc(af_weights* w, const int32_t* token_ids, const void* embeds, int32_t M,
+                                    const af_segment* segs, int32_t n_seg, af_ring* ring, void* out_hidden,
+                                    float* out_logits, int32_t* out_tokens, void* hip_stream);
 
 /* ------------------------------------------------------------------ single steps of the path
  * Each runs one step of Alg. 2 / Alg. 1 on caller buffers with the same kernels the forward

@@ -80,6 +80,7 @@ def _load():
         "af_weights_create": (I32, [C.POINTER(ModelDesc), PP, I32, P, PP]),
         "af_weights_destroy": (I32, [P]),
         "af_packed_forward": (I32, [P, P, P, I32, SEG, I32, P, P, P, P, P]),
+        "af_packed_forward_noalloc": (I32, [P, P, P, I32, SEG, I32, P, P, P, P, P]),
         "af_packed_layer_forward": (I32, [P, I32, P, I32, SEG, I32, P, P]),
         "af_packed_layer_forward_kv": (I32, [P, I32, P, I32, SEG, I32, P, I32, P]),
         "af_weights_device_errors": (I32, [P, P, C.POINTER(I32)]),
@@ -272,6 +273,15 @@ def packed_forward(w: Weights, token_ids: torch.Tensor, embeds: Optional[torch.T
     sa = segs if isinstance(segs, C.Array) else segments_array(segs)
     _check(lib.af_packed_forward(w.h, _ptr(token_ids), _ptr(embeds), token_ids.shape[0], sa, len(sa), ring.h,
                                  _ptr(out_hidden), _ptr(out_logits), _ptr(out_tokens), _stream(stream)))
+
+
+def packed_forward_noalloc(w: Weights, token_ids: torch.Tensor, embeds: Optional[torch.Tensor], segs, ring: Ring,
+                           out_hidden: torch.Tensor, out_logits: Optional[torch.Tensor] = None,
+                           out_tokens: Optional[torch.Tensor] = None, stream=None):
+    """packed_forward with the library's fixed per-GPU scratch array instead of allocations."""
+    sa = segs if isinstance(segs, C.Array) else segments_array(segs)
+    _check(lib.af_packed_forward_noalloc(w.h, _ptr(token_ids), _ptr(embeds), token_ids.shape[0], sa, len(sa), ring.h,
+                                         _ptr(out_hidden), _ptr(out_logits), _ptr(out_tokens), _stream(stream)))
 
 
 def packed_layer_forward(w: Weights, layer: int, hidden: torch.Tensor, segs, ring: Ring, stream=None,

@@ -13,7 +13,7 @@ CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libactionflow.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
-HIP_SOURCES = ["af_kernels.hip"]
+HIP_SOURCES = ["af_kernels.hip", "af_noalloc.hip"]
 HOST_SOURCES = ["af_ring.cpp", "af_model.cpp"]
 
 # Packed-fp32 instructions are disabled for all device code (hipcc makes them from plain float

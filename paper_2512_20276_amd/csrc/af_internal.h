@@ -98,6 +98,8 @@ hipError_t launch_to_frag(int dtype, const void* x, int ld, int M, int K, int Kp
 hipError_t launch_embed(int dtype, const int32_t* ids, const void* table, int vocab, const void* embeds, void* out,
                         int M, int D, int32_t* err_count, hipStream_t s);
 hipError_t launch_argmax(const float* logits, int n_rows, int V, int32_t* tokens, hipStream_t s);
+// Zero-fills n_runs runs of run_bytes (16-byte multiple, 16-byte aligned), run r at base + r * stride.
+hipError_t launch_zero_runs(void* base, int n_runs, size_t stride, size_t run_bytes, hipStream_t s);
 // Byte strides of a run copy: run r starts at (r / per_group) * group + (r % per_group) * run.
 struct CopyStrides {
   size_t src_group, src_run, dst_group, dst_run;
@@ -134,6 +136,20 @@ constexpr int ATTN_BQ = 64;   // query rows per attention work tile
 constexpr int ATTN_WAVES = 8; // waves per attention workgroup (two key groups of four for query tiles)
 constexpr int ATTN_BKV = 64;  // keys per LDS tile
 constexpr int MAX_SEGMENTS = 4096;
+
+// Which rotary table a caller-free buffer holds: angles pos * theta^(-2j/hd) for rows
+// [0, rows) (rows = 0: none).
+struct BufferRope {
+  float theta = 0.f;
+  int head_dim = 0;
+  int rows = 0;
+};
+// af_packed_forward with every device workspace carved from buf (buf_bytes), allocating
+// nothing; a step that does not fit is AF_ERR_OUT_OF_RANGE before any launch.
+af_status packed_forward_in_buffer(af_weights* w, const int32_t* token_ids, const void* embeds, int32_t M,
+                                   const af_segment* segs, int32_t n_seg, af_ring* ring, void* out_hidden,
+                                   float* out_logits, int32_t* out_tokens, hipStream_t s, void* buf,
+                                   size_t buf_bytes, BufferRope* rope);
 
 }  // namespace af
 

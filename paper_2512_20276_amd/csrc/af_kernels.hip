@@ -1732,6 +1732,23 @@ hipError_t launch_run_copy(void* base, size_t src, size_t dst, int n_runs, int p
   return launch_copy_runs((const char*)base + src, (char*)base + dst, n_runs, per_group, st, run_bytes, s);
 }
 
+__global__ __launch_bounds__(256) void zero_runs_kernel(char* base, size_t stride, size_t run_bytes) {
+  uint4* p = (uint4*)(base + (size_t)blockIdx.x * stride);
+  const size_t n16 = run_bytes / 16, chunk = (size_t)blockIdx.y * 4096;  // 64 KiB per block
+  const size_t end = n16 < chunk + 4096 ? n16 : chunk + 4096;
+  for (size_t i = chunk + threadIdx.x; i < end; i += 256) p[i] = zero4();
+}
+
+hipError_t launch_zero_runs(void* base, int n_runs, size_t stride, size_t run_bytes, hipStream_t s) {
+  if (n_runs <= 0 || run_bytes == 0) return hipSuccess;
+  if (run_bytes % 16 || (uintptr_t)base % 16 || stride % 16) return hipErrorInvalidValue;
+  const size_t chunks = (run_bytes / 16 + 4095) / 4096;
+  if (chunks > 65535) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(zero_runs_kernel, dim3(n_runs, (unsigned)chunks), dim3(256), 0, s, (char*)base, stride,
+                     run_bytes);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ weight repacking
 // dst: fragment-tiled [N/16][Kp/32][64 lanes][8] (see the GEMM); source row n is
 // srcs[map[2n]] row map[2n+1] (or src0 row n without a map), rows of K elements, k >= K zero.

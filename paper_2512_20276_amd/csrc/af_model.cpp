@@ -81,6 +81,21 @@ struct af_weights {
 
 namespace {
 
+// Device workspace of one forward call.  The allocating entry points take it from the weights
+// object (grown on demand, `grow` set); the no-allocation entry point carves it from a fixed
+// buffer (`grow` null: a split-K partial buffer that is too small is an error, not a resize).
+// `timing` is the weights object whose timing mask applies, or null for no timing.
+struct Ws {
+  af_weights* grow = nullptr;
+  af_weights* timing = nullptr;
+  void *xn = nullptr, *q = nullptr, *attn = nullptr, *act = nullptr, *emit_norm = nullptr;
+  float* logits = nullptr;  // fp32 logits of the emitting rows when the caller passes none
+  int32_t* desc = nullptr;  // the uploaded step tables
+  const float* rope = nullptr;
+  float* partial = nullptr;
+  size_t partial_cap = 0;   // floats
+};
+
 af_status dev_alloc(af_weights* w, void** p, size_t bytes) {
   hipError_t e = hipMalloc(p, bytes);
   if (e != hipSuccess) {
@@ -357,6 +372,23 @@ af_status ensure_rope(af_weights* w, int max_pos) {
   return AF_OK;
 }
 
+Ws ws_of(af_weights* w) {
+  Ws ws;
+  ws.grow = w;
+  ws.timing = w;
+  ws.xn = w->xn;
+  ws.q = w->q;
+  ws.attn = w->attn;
+  ws.act = w->act;
+  ws.emit_norm = w->emit_norm;
+  ws.logits = w->logits_ws;
+  ws.desc = w->desc_dev;
+  ws.rope = w->rope_cs;
+  ws.partial = w->partial;
+  ws.partial_cap = w->partial_cap;
+  return ws;
+}
+
 // ---------------------------------------------------------------- timed launches
 hipEvent_t take_event(af_weights* w) {
   if (!w->event_pool.empty()) {
@@ -403,12 +435,12 @@ struct DevTables {
   int n_tiles, n_multi, n_emit;
 };
 
-DevTables dev_tables(const af_weights* w, const StepDesc& sd) {
+DevTables dev_tables(const int32_t* desc, const StepDesc& sd) {
   DevTables t;
-  t.segs = (const DevSeg*)(w->desc_dev + sd.off_segs);
-  t.row_sp = w->desc_dev + sd.off_rows;
-  t.tiles = w->desc_dev + sd.off_tiles;
-  t.emit_rows = w->desc_dev + sd.off_emit;
+  t.segs = (const DevSeg*)(desc + sd.off_segs);
+  t.row_sp = desc + sd.off_rows;
+  t.tiles = desc + sd.off_tiles;
+  t.emit_rows = desc + sd.off_emit;
   t.n_tiles = sd.n_tiles;
   t.n_multi = sd.n_multi;
   t.n_emit = sd.n_emit;
@@ -435,43 +467,56 @@ GemmArgs gemm_args(int dtype, const void* A, int lda, long astride, const void* 
   return g;
 }
 
-af_status with_splits(af_weights* w, GemmArgs& g) {
+// fp32 elements of split-K partial sums a GEMM of this shape needs (0: no split).
+size_t split_need(const af_weights* w, int M, int N, int K) {
+  if (w->options & AF_OPT_NO_SPLIT_K) return 0;
+  const int S = gemm_splits(w->d.dtype, M, N, padk(K));
+  return S > 1 ? (size_t)S * M * N : 0;
+}
+
+af_status with_splits(af_weights* w, Ws& ws, GemmArgs& g) {
   if (!w || (w->options & AF_OPT_NO_SPLIT_K)) return AF_OK;
   const int S = gemm_splits(w->d.dtype, g.M, g.N, g.Kp);
   if (S <= 1) return AF_OK;
   const size_t need = (size_t)S * g.M * g.N;
-  if (need > w->partial_cap) {
+  if (need > ws.partial_cap) {
+    if (!ws.grow) {
+      set_error("split-K partial buffer too small (%zu floats, need %zu)", ws.partial_cap, need);
+      return AF_ERR_OUT_OF_RANGE;
+    }
     AF_HIP(hipDeviceSynchronize());
     dev_free(w, w->partial);
     w->partial = nullptr;
     w->partial_cap = 0;
     AF_TRY(dev_alloc(w, (void**)&w->partial, need * 4));
     w->partial_cap = need;
+    ws.partial = w->partial;
+    ws.partial_cap = need;
   }
   g.splits = S;
-  g.partial = w->partial;
+  g.partial = ws.partial;
   return AF_OK;
 }
 
 // l: the weights' layer; rl: the ring layer that holds this layer's keys and values.
-af_status step_qkv(af_weights* w, int l, const void* xn, int ldx, long xs, int M, af_ring* ring, int rl, const DevTables& t,
-                   void* q_out, int ldq, hipStream_t s) {
+af_status step_qkv(af_weights* w, Ws& ws, int l, const void* xn, int ldx, long xs, int M, af_ring* ring, int rl,
+                   const DevTables& t, void* q_out, int ldq, hipStream_t s) {
   const af_model_desc& d = w->d;
   GemmArgs g = gemm_args(d.dtype, xn, ldx, xs, w->layers[l].wqkv, M, 3 * d.d_model, d.d_model, q_out, ldq);
   const size_t es = w->es;
   g.ring_k = (char*)ring->kv + ring->offset(rl, 0, 0, 0, 0) * es;
   g.ring_v = (char*)ring->kv + ring->offset(rl, 1, 0, 0, 0) * es;
   g.row_sp = t.row_sp;
-  g.rope_cs = w->rope_cs;
+  g.rope_cs = ws.rope;
   g.d_model = d.d_model;
   g.head_dim = d.head_dim;
   g.n_heads = d.n_heads;
   g.max_pos = ring->d.max_pos;
-  AF_TRY(with_splits(w, g));
-  return timed(w, AF_K_GEMM_QKV, s, [&] { return launch_gemm(d.dtype, EPI_QKV, g, s); });
+  AF_TRY(with_splits(w, ws, g));
+  return timed(ws.timing, AF_K_GEMM_QKV, s, [&] { return launch_gemm(d.dtype, EPI_QKV, g, s); });
 }
 
-af_status step_attention(af_weights* w, int dtype, af_ring* ring, int l, const void* q, int ldq, void* o, int ldo,
+af_status step_attention(af_weights* tw, int dtype, af_ring* ring, int l, const void* q, int ldq, void* o, int ldo,
                          long os, const DevTables& t, hipStream_t s) {
   AttnArgs a;
   std::memset(&a, 0, sizeof(a));
@@ -489,96 +534,97 @@ af_status step_attention(af_weights* w, int dtype, af_ring* ring, int l, const v
   a.ldo = ldo;
   a.ostride = os;
   a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)ring->d.head_dim));
-  return timed(w, AF_K_ATTENTION, s, [&] { return launch_attention(dtype, ring->d.head_dim, a, t.n_tiles, s); });
+  return timed(tw, AF_K_ATTENTION, s, [&] { return launch_attention(dtype, ring->d.head_dim, a, t.n_tiles, s); });
 }
 
 // Residual projections (output and down).  With split-K and a norm gain, the partial sums, the
-// residual update and the RMSNorm of the updated rows (gain `norm`, into w->xn) run as one
+// residual update and the RMSNorm of the updated rows (gain `norm`, into ws.xn) run as one
 // kernel after the GEMM; *normed tells the caller whether that norm was produced.
-af_status step_resid_proj(af_weights* w, int cls, const void* A, int lda, long as, const void* W, int K, void* hidden,
-                          int M, const void* norm, bool* normed, hipStream_t s) {
+af_status step_resid_proj(af_weights* w, Ws& ws, int cls, const void* A, int lda, long as, const void* W, int K,
+                          void* hidden, int M, const void* norm, bool* normed, hipStream_t s) {
   const af_model_desc& d = w->d;
   GemmArgs g = gemm_args(d.dtype, A, lda, as, W, M, d.d_model, K, hidden, d.d_model);
   g.resid = hidden;
   g.ldr = d.d_model;
-  AF_TRY(with_splits(w, g));
+  AF_TRY(with_splits(w, ws, g));
   *normed = norm && g.splits > 1;
-  if (!*normed) return timed(w, cls, s, [&] { return launch_gemm(d.dtype, EPI_RESID, g, s); });
+  if (!*normed) return timed(ws.timing, cls, s, [&] { return launch_gemm(d.dtype, EPI_RESID, g, s); });
   g.partials_only = 1;
-  return timed(w, cls, s, [&] {
+  return timed(ws.timing, cls, s, [&] {
     hipError_t e = launch_gemm(d.dtype, EPI_RESID, g, s);
     if (e != hipSuccess) return e;
-    return launch_resid_norm(d.dtype, g.partial, g.splits, hidden, d.d_model, norm, w->xn, w->ldD, w->xs_D, M,
+    return launch_resid_norm(d.dtype, g.partial, g.splits, hidden, d.d_model, norm, ws.xn, w->ldD, w->xs_D, M,
                              d.d_model, d.rms_eps, s);
   });
 }
 
-af_status step_o(af_weights* w, int l, const void* o, int ldo_in, long os, void* hidden, int M, hipStream_t s,
+af_status step_o(af_weights* w, Ws& ws, int l, const void* o, int ldo_in, long os, void* hidden, int M, hipStream_t s,
                  const void* norm = nullptr, bool* normed = nullptr) {
   bool dummy;
-  return step_resid_proj(w, AF_K_GEMM_O, o, ldo_in, os, w->layers[l].wo, w->d.d_model, hidden, M, norm,
+  return step_resid_proj(w, ws, AF_K_GEMM_O, o, ldo_in, os, w->layers[l].wo, w->d.d_model, hidden, M, norm,
                          normed ? normed : &dummy, s);
 }
 
-af_status step_gate_up(af_weights* w, int l, const void* xn, int ldx, long xs, void* act, int ld_act, long act_os,
-                       int M, hipStream_t s) {
+af_status step_gate_up(af_weights* w, Ws& ws, int l, const void* xn, int ldx, long xs, void* act, int ld_act,
+                       long act_os, int M, hipStream_t s) {
   const af_model_desc& d = w->d;
   GemmArgs g = gemm_args(d.dtype, xn, ldx, xs, w->layers[l].wgu, M, 2 * d.d_ff, d.d_model, act, ld_act);
   g.ostride = act_os;
-  AF_TRY(with_splits(w, g));
-  return timed(w, AF_K_GEMM_GATEUP, s, [&] { return launch_gemm(d.dtype, EPI_SWIGLU, g, s); });
+  AF_TRY(with_splits(w, ws, g));
+  return timed(ws.timing, AF_K_GEMM_GATEUP, s, [&] { return launch_gemm(d.dtype, EPI_SWIGLU, g, s); });
 }
 
-af_status step_down(af_weights* w, int l, const void* act, int ld_act, long as, void* hidden, int M, hipStream_t s,
-                    const void* norm = nullptr, bool* normed = nullptr) {
+af_status step_down(af_weights* w, Ws& ws, int l, const void* act, int ld_act, long as, void* hidden, int M,
+                    hipStream_t s, const void* norm = nullptr, bool* normed = nullptr) {
   bool dummy;
-  return step_resid_proj(w, AF_K_GEMM_DOWN, act, ld_act, as, w->layers[l].wdown, w->d.d_ff, hidden, M, norm,
+  return step_resid_proj(w, ws, AF_K_GEMM_DOWN, act, ld_act, as, w->layers[l].wdown, w->d.d_ff, hidden, M, norm,
                          normed ? normed : &dummy, s);
 }
 
-af_status step_norm(af_weights* w, const void* x, int ldx, const int32_t* rows, const void* g, void* y, int ldy,
-                    long ys, int n_rows, hipStream_t s) {
+af_status step_norm(af_weights* w, af_weights* tw, const void* x, int ldx, const int32_t* rows, const void* g,
+                    void* y, int ldy, long ys, int n_rows, hipStream_t s) {
   const af_model_desc& d = w->d;
-  return timed(w, AF_K_RMSNORM, s, [&] {
+  return timed(tw, AF_K_RMSNORM, s, [&] {
     return launch_rmsnorm(d.dtype, x, ldx, rows, g, y, ldy, ys, n_rows, d.d_model, d.rms_eps, s);
   });
 }
 
 // One decoder layer (Alg. 2).  xn_ready: the previous layer's down projection already wrote
-// this layer's attention-normed rows into w->xn.  next_norm: the next layer's attention-norm
+// this layer's attention-normed rows into ws.xn.  next_norm: the next layer's attention-norm
 // gain, which this layer's down projection applies when it can (*next_ready then says so).
 // Layer l of the weights; its keys and values live in ring layer rl.
-af_status layer_forward(af_weights* w, int l, void* hidden, int M, af_ring* ring, int rl, const DevTables& t,
+af_status layer_forward(af_weights* w, Ws& ws, int l, void* hidden, int M, af_ring* ring, int rl, const DevTables& t,
                         hipStream_t s, bool xn_ready = false, const void* next_norm = nullptr,
                         bool* next_ready = nullptr) {
   const Layer& L = w->layers[l];
   const int D = w->d.d_model, ldD = w->ldD, ldF = w->ldF;
   const long xD = w->xs_D, xF = w->xs_F;  // 0 (row-major) for fp32
-  if (!xn_ready) AF_TRY(step_norm(w, hidden, D, nullptr, L.attn_norm, w->xn, ldD, xD, M, s));
-  AF_TRY(step_qkv(w, l, w->xn, ldD, xD, M, ring, rl, t, w->q, ldD, s));
-  AF_TRY(step_attention(w, w->d.dtype, ring, rl, w->q, ldD, w->attn, ldD, xD, t, s));
+  if (!xn_ready) AF_TRY(step_norm(w, ws.timing, hidden, D, nullptr, L.attn_norm, ws.xn, ldD, xD, M, s));
+  AF_TRY(step_qkv(w, ws, l, ws.xn, ldD, xD, M, ring, rl, t, ws.q, ldD, s));
+  AF_TRY(step_attention(ws.timing, w->d.dtype, ring, rl, ws.q, ldD, ws.attn, ldD, xD, t, s));
   // InPlaceKVShift: no device work; the slot rotation lives in the ring bookkeeping.
   bool mlp_normed = false;
-  AF_TRY(step_o(w, l, w->attn, ldD, xD, hidden, M, s, L.mlp_norm, &mlp_normed));
-  if (!mlp_normed) AF_TRY(step_norm(w, hidden, D, nullptr, L.mlp_norm, w->xn, ldD, xD, M, s));
-  AF_TRY(step_gate_up(w, l, w->xn, ldD, xD, w->act, ldF, xF, M, s));
+  AF_TRY(step_o(w, ws, l, ws.attn, ldD, xD, hidden, M, s, L.mlp_norm, &mlp_normed));
+  if (!mlp_normed) AF_TRY(step_norm(w, ws.timing, hidden, D, nullptr, L.mlp_norm, ws.xn, ldD, xD, M, s));
+  AF_TRY(step_gate_up(w, ws, l, ws.xn, ldD, xD, ws.act, ldF, xF, M, s));
   bool dummy;
-  AF_TRY(step_down(w, l, w->act, ldF, xF, hidden, M, s, next_norm, next_ready ? next_ready : &dummy));
+  AF_TRY(step_down(w, ws, l, ws.act, ldF, xF, hidden, M, s, next_norm, next_ready ? next_ready : &dummy));
   return AF_OK;
 }
 
-af_status lm_head(af_weights* w, const void* hidden, const DevTables& t, float* out_logits, int32_t* out_tokens,
-                  hipStream_t s) {
+af_status lm_head(af_weights* w, Ws& ws, const void* hidden, const DevTables& t, float* out_logits,
+                  int32_t* out_tokens, hipStream_t s) {
   const af_model_desc& d = w->d;
   if (t.n_emit == 0 || (!out_logits && !out_tokens)) return AF_OK;
-  AF_TRY(step_norm(w, hidden, d.d_model, t.emit_rows, w->final_norm, w->emit_norm, w->ldD, w->xs_D, t.n_emit, s));
-  float* logits = out_logits ? out_logits : w->logits_ws;
-  GemmArgs g = gemm_args(d.dtype, w->emit_norm, w->ldD, w->xs_D, w->lm_head, t.n_emit, d.vocab, d.d_model, logits,
+  AF_TRY(step_norm(w, ws.timing, hidden, d.d_model, t.emit_rows, w->final_norm, ws.emit_norm, w->ldD, w->xs_D,
+                   t.n_emit, s));
+  float* logits = out_logits ? out_logits : ws.logits;
+  GemmArgs g = gemm_args(d.dtype, ws.emit_norm, w->ldD, w->xs_D, w->lm_head, t.n_emit, d.vocab, d.d_model, logits,
                          d.vocab);
-  AF_TRY(with_splits(w, g));
-  AF_TRY(timed(w, AF_K_LM_HEAD, s, [&] { return launch_gemm(d.dtype, EPI_STORE_F32, g, s); }));
+  AF_TRY(with_splits(w, ws, g));
+  AF_TRY(timed(ws.timing, AF_K_LM_HEAD, s, [&] { return launch_gemm(d.dtype, EPI_STORE_F32, g, s); }));
   if (out_tokens)
-    AF_TRY(timed(w, AF_K_ARGMAX, s, [&] { return launch_argmax(logits, t.n_emit, d.vocab, out_tokens, s); }));
+    AF_TRY(timed(ws.timing, AF_K_ARGMAX, s, [&] { return launch_argmax(logits, t.n_emit, d.vocab, out_tokens, s); }));
   return AF_OK;
 }
 
@@ -590,6 +636,37 @@ af_status prepare_step(af_weights* w, af_ring* ring, const af_segment* segs, int
   AF_TRY(ensure_workspace(w, M, sd.n_emit));
   AF_TRY(ensure_rope(w, ring->d.max_pos));
   AF_TRY(upload_desc(w, sd, s));
+  return AF_OK;
+}
+
+// The whole step (Alg. 1 Embed .. ArgMax) on a prepared workspace and uploaded tables.
+af_status forward_steps(af_weights* w, Ws& ws, const DevTables& t, const int32_t* token_ids, const void* embeds,
+                        int M, af_ring* ring, void* out_hidden, float* out_logits, int32_t* out_tokens,
+                        hipStream_t s) {
+  const af_model_desc& d = w->d;
+  AF_TRY(timed(ws.timing, AF_K_EMBED, s, [&] {
+    return launch_embed(d.dtype, token_ids, w->embed, d.vocab, embeds, out_hidden, M, d.d_model, w->dev_err, s);
+  }));
+  bool xn_ready = false;
+  for (int l = 0; l < d.n_layers; ++l) {
+    const void* next = l + 1 < d.n_layers ? w->layers[l + 1].attn_norm : nullptr;
+    bool next_ready = false;
+    AF_TRY(layer_forward(w, ws, l, out_hidden, M, ring, l, t, s, xn_ready, next, &next_ready));
+    xn_ready = next_ready;
+  }
+  return lm_head(w, ws, out_hidden, t, out_logits, out_tokens, s);
+}
+
+af_status check_forward_args(const af_weights* w, const int32_t* token_ids, const void* out_hidden,
+                             const af_ring* ring) {
+  if (!w || !token_ids || !out_hidden) {
+    set_error("af_packed_forward: weights, token_ids and out_hidden must be non-NULL");
+    return AF_ERR_INVALID_ARG;
+  }
+  if (ring && ring->d.n_layers != w->d.n_layers) {
+    set_error("af_packed_forward: ring has %d layers, model %d", ring->d.n_layers, w->d.n_layers);
+    return AF_ERR_INVALID_ARG;
+  }
   return AF_OK;
 }
 
@@ -759,30 +836,13 @@ extern "C" af_status af_packed_forward(af_weights* w, const int32_t* token_ids, 
                                        const af_segment* segs, int32_t n_seg, af_ring* ring, void* out_hidden,
                                        float* out_logits, int32_t* out_tokens, void* hip_stream) {
   clear_error();
-  if (!w || !token_ids || !out_hidden) {
-    set_error("af_packed_forward: weights, token_ids and out_hidden must be non-NULL");
-    return AF_ERR_INVALID_ARG;
-  }
-  if (ring && ring->d.n_layers != w->d.n_layers) {
-    set_error("af_packed_forward: ring has %d layers, model %d", ring->d.n_layers, w->d.n_layers);
-    return AF_ERR_INVALID_ARG;
-  }
+  AF_TRY(check_forward_args(w, token_ids, out_hidden, ring));
   hipStream_t s = (hipStream_t)hip_stream;
   StepDesc sd;
   AF_TRY(prepare_step(w, ring, segs, n_seg, M, w->d.n_layers, sd, s));
-  const DevTables t = dev_tables(w, sd);
-  const af_model_desc& d = w->d;
-  AF_TRY(timed(w, AF_K_EMBED, s, [&] {
-    return launch_embed(d.dtype, token_ids, w->embed, d.vocab, embeds, out_hidden, M, d.d_model, w->dev_err, s);
-  }));
-  bool xn_ready = false;
-  for (int l = 0; l < d.n_layers; ++l) {
-    const void* next = l + 1 < d.n_layers ? w->layers[l + 1].attn_norm : nullptr;
-    bool next_ready = false;
-    AF_TRY(layer_forward(w, l, out_hidden, M, ring, l, t, s, xn_ready, next, &next_ready));
-    xn_ready = next_ready;
-  }
-  return lm_head(w, out_hidden, t, out_logits, out_tokens, s);
+  Ws ws = ws_of(w);
+  return forward_steps(w, ws, dev_tables(ws.desc, sd), token_ids, embeds, M, ring, out_hidden, out_logits,
+                       out_tokens, s);
 }
 
 extern "C" af_status af_packed_layer_forward(af_weights* w, int32_t layer, void* hidden_inout, int32_t M,
@@ -810,7 +870,96 @@ extern "C" af_status af_packed_layer_forward_kv(af_weights* w, int32_t layer, vo
   hipStream_t s = (hipStream_t)hip_stream;
   StepDesc sd;
   AF_TRY(prepare_step(w, ring, segs, n_seg, M, ring_layer + 1, sd, s));
-  return layer_forward(w, layer, hidden_inout, M, ring, ring_layer, dev_tables(w, sd), s);
+  Ws ws = ws_of(w);
+  return layer_forward(w, ws, layer, hidden_inout, M, ring, ring_layer, dev_tables(ws.desc, sd), s);
+}
+
+// ================================================================ forward in a caller-free buffer
+// The step of af_packed_forward with every device workspace carved from one fixed buffer: no
+// device or pinned-host allocation.  Layout (256-byte aligned regions): rotary table, step
+// tables, xn, attn, act, q, emit_norm, fp32 logits (only when tokens are wanted without
+// logits), split-K partials (the largest any GEMM of the step needs).  The rotary table is
+// uploaded only when *rope says the buffer does not already hold it.
+af_status af::packed_forward_in_buffer(af_weights* w, const int32_t* token_ids, const void* embeds, int32_t M,
+                                       const af_segment* segs, int32_t n_seg, af_ring* ring, void* out_hidden,
+                                       float* out_logits, int32_t* out_tokens, hipStream_t s, void* buf,
+                                       size_t buf_bytes, BufferRope* rope) {
+  AF_TRY(check_forward_args(w, token_ids, out_hidden, ring));
+  AF_TRY(check_ring_matches(w, ring, w->d.n_layers));
+  AF_TRY(check_segments(ring, segs, n_seg, M));
+  const af_model_desc& d = w->d;
+  StepDesc sd;
+  build_desc(segs, n_seg, M, sd);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += (bytes + 255) / 256 * 256;
+    return o;
+  };
+  const int half = d.head_dim / 2, max_pos = ring->d.max_pos;
+  const size_t o_rope = take((size_t)max_pos * half * 2 * 4);
+  const size_t o_desc = take(sd.buf.size() * 4);
+  const size_t o_xn = take(act_bytes(w, M, false));
+  const size_t o_attn = take(act_bytes(w, M, false));
+  const size_t o_act = take(act_bytes(w, M, true));
+  const size_t o_q = take((size_t)M * w->ldD * w->es);
+  const int n_emit = sd.n_emit;
+  const size_t o_emit = take(act_bytes(w, std::max(n_emit, 1), false));
+  const bool head = n_emit > 0 && (out_logits || out_tokens);
+  const size_t o_logits = take(head && !out_logits ? (size_t)n_emit * d.vocab * 4 : 0);
+  size_t part = std::max({split_need(w, M, 3 * d.d_model, d.d_model), split_need(w, M, d.d_model, d.d_model),
+                          split_need(w, M, 2 * d.d_ff, d.d_model), split_need(w, M, d.d_model, d.d_ff)});
+  if (head) part = std::max(part, split_need(w, n_emit, d.vocab, d.d_model));
+  const size_t o_part = take(part * 4);
+  if (off > buf_bytes) {
+    set_error("af_packed_forward_noalloc: this step needs %zu bytes of scratch (M = %d, d_model %d, d_ff %d, "
+              "ring max_pos %d, %d emitting rows); the library holds %zu",
+              off, M, d.d_model, d.d_ff, max_pos, n_emit, buf_bytes);
+    return AF_ERR_OUT_OF_RANGE;
+  }
+  char* base = (char*)buf;
+  if (!(rope->theta == d.rope_theta && rope->head_dim == d.head_dim && rope->rows >= max_pos)) {
+    std::vector<float> t((size_t)max_pos * half * 2);
+    for (int p = 0; p < max_pos; ++p)
+      for (int j = 0; j < half; ++j) {
+        const double ang = (double)p * std::pow((double)d.rope_theta, -2.0 * j / d.head_dim);
+        t[((size_t)p * half + j) * 2] = (float)std::cos(ang);
+        t[((size_t)p * half + j) * 2 + 1] = (float)std::sin(ang);
+      }
+    rope->rows = 0;
+    AF_HIP(hipMemcpyAsync(base + o_rope, t.data(), t.size() * 4, hipMemcpyHostToDevice, s));
+  }
+  rope->theta = d.rope_theta;
+  rope->head_dim = d.head_dim;
+  rope->rows = max_pos;  // what lies past this call's table may be overwritten by its other regions
+  AF_HIP(hipMemcpyAsync(base + o_desc, sd.buf.data(), sd.buf.size() * 4, hipMemcpyHostToDevice, s));
+  Ws ws;
+  ws.xn = base + o_xn;
+  ws.attn = base + o_attn;
+  ws.act = base + o_act;
+  ws.q = base + o_q;
+  ws.emit_norm = base + o_emit;
+  ws.logits = (float*)(base + o_logits);
+  ws.desc = (int32_t*)(base + o_desc);
+  ws.rope = (const float*)(base + o_rope);
+  ws.partial = part ? (float*)(base + o_part) : nullptr;
+  ws.partial_cap = part;
+  if (d.dtype == AF_BF16) {
+    // the fragment-tiled GEMM inputs read k up to the padded K: those columns must be zero
+    auto zero_pad = [&](void* p, int rows, int K, long xs) -> af_status {
+      const int Kp = padk(K);
+      if (Kp == K) return AF_OK;
+      const size_t head_bytes = (size_t)(K / 16) * 512 * 2, pad_bytes = (size_t)((Kp - K) / 16) * 512 * 2;
+      AF_HIP(launch_zero_runs((char*)p + head_bytes, (rows + 31) / 32, (size_t)xs * 2, pad_bytes, s));
+      return AF_OK;
+    };
+    AF_TRY(zero_pad(ws.xn, M, d.d_model, w->xs_D));
+    AF_TRY(zero_pad(ws.attn, M, d.d_model, w->xs_D));
+    AF_TRY(zero_pad(ws.act, M, d.d_ff, w->xs_F));
+    AF_TRY(zero_pad(ws.emit_norm, std::max(n_emit, 1), d.d_model, w->xs_D));
+  }
+  return forward_steps(w, ws, dev_tables(ws.desc, sd), token_ids, embeds, M, ring, out_hidden, out_logits,
+                       out_tokens, s);
 }
 
 // ================================================================ single steps
@@ -910,7 +1059,9 @@ extern "C" af_status af_op_qkv_rope_write(af_weights* w, int32_t layer, const vo
   StepDesc sd;
   AF_TRY(prepare_step(w, ring, segs, n_seg, M, layer + 1, sd, s));
   AF_TRY(stage_input(w, xn, w->d.d_model, M, w->xn, w->xs_D, s));
-  return step_qkv(w, layer, xn, w->d.d_model, w->xs_D, M, ring, layer, dev_tables(w, sd), q_out, w->d.d_model, s);
+  Ws ws = ws_of(w);
+  return step_qkv(w, ws, layer, xn, w->d.d_model, w->xs_D, M, ring, layer, dev_tables(ws.desc, sd), q_out,
+                  w->d.d_model, s);
 }
 
 extern "C" af_status af_op_attention(af_ring* ring, int32_t layer, const void* q, int32_t M, const af_segment* segs,
@@ -960,7 +1111,8 @@ extern "C" af_status af_op_o_proj_residual(af_weights* w, int32_t layer, const v
   hipStream_t s = (hipStream_t)hip_stream;
   AF_TRY(ensure_workspace(w, M, 0));
   AF_TRY(stage_input(w, o, w->d.d_model, M, w->attn, w->xs_D, s));
-  return step_o(w, layer, o, w->d.d_model, w->xs_D, hidden, M, s);
+  Ws ws = ws_of(w);
+  return step_o(w, ws, layer, o, w->d.d_model, w->xs_D, hidden, M, s);
 }
 
 extern "C" af_status af_op_gate_up_swiglu(af_weights* w, int32_t layer, const void* xn, void* act, int32_t M,
@@ -973,7 +1125,8 @@ extern "C" af_status af_op_gate_up_swiglu(af_weights* w, int32_t layer, const vo
   hipStream_t s = (hipStream_t)hip_stream;
   AF_TRY(ensure_workspace(w, M, 0));
   AF_TRY(stage_input(w, xn, w->d.d_model, M, w->xn, w->xs_D, s));
-  return step_gate_up(w, layer, xn, w->d.d_model, w->xs_D, act, w->d.d_ff, 0, M, s);
+  Ws ws = ws_of(w);
+  return step_gate_up(w, ws, layer, xn, w->d.d_model, w->xs_D, act, w->d.d_ff, 0, M, s);
 }
 
 extern "C" af_status af_op_down_residual(af_weights* w, int32_t layer, const void* act, void* hidden, int32_t M,
@@ -986,7 +1139,8 @@ extern "C" af_status af_op_down_residual(af_weights* w, int32_t layer, const voi
   hipStream_t s = (hipStream_t)hip_stream;
   AF_TRY(ensure_workspace(w, M, 0));
   AF_TRY(stage_input(w, act, w->d.d_ff, M, w->act, w->xs_F, s));
-  return step_down(w, layer, act, w->d.d_ff, w->xs_F, hidden, M, s);
+  Ws ws = ws_of(w);
+  return step_down(w, ws, layer, act, w->d.d_ff, w->xs_F, hidden, M, s);
 }
 
 extern "C" af_status af_op_lm_head_argmax(af_weights* w, const void* hidden, int32_t M, const af_segment* segs,
@@ -1006,7 +1160,8 @@ extern "C" af_status af_op_lm_head_argmax(af_weights* w, const void* hidden, int
   build_desc(segs, n_seg, M, sd);
   AF_TRY(ensure_workspace(w, M, sd.n_emit));
   AF_TRY(upload_desc(w, sd, s));
-  return lm_head(w, hidden, dev_tables(w, sd), out_logits, out_tokens, s);
+  Ws ws = ws_of(w);
+  return lm_head(w, ws, hidden, dev_tables(ws.desc, sd), out_logits, out_tokens, s);
 }
 
 extern "C" af_status af_weights_set_options(af_weights* w, uint32_t flags) {
