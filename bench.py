@@ -45,7 +45,7 @@ def parse():
     p.add_argument("--steps", type=int, default=30)
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
+    p.add_argument("--cpu-steps", type=int, default=2, help="whole 32-layer steps of the CPU oracle sample")
     p.add_argument("--no-timing-pass", action="store_true")
     p.add_argument("--no-extra", action="store_true",
                    help="skip the measurements beside the packed step (baseline, attention, sweeps, ablations)")
@@ -66,7 +66,7 @@ def parse():
 
 
 COPY_BYTES = 1 << 30        # calibration copy: 1 GiB read + 1 GiB written, far beyond the 256 MB last-level cache
-KERNELS_SRC = os.path.join(ROOT, "paper_2512_20276_amd", "csrc", "af_kernels.hip")
+KERNELS_SRC = os.path.join(ROOT, "paper_2512_20276_amd", "csrc", "af_gemm.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_gemm_gateup_7b_m282.md")
 
 
@@ -424,39 +424,45 @@ def stress(af, w, shape, steps=8):
             "kernel_ms_per_step": {k: round(ms / steps, 4) for k, (ms, n) in tm.items()}}
 
 
-def k_sweep(af, w, shape, pids, Ks=(7, 16, 24, 32), steps=12):
-    """Action length K swept as in the paper's K experiment: the 32-layer pipeline at each K
-    (one 276-row prefill + K - 1 decode rows per step, ring K + 1 slots), against the plain
-    per-request schedule on the same kernels (prefill, then K - 1 single-row decodes)."""
+def k_sweep(af, w, shape, Ks=(7, 16, 24, 32), text_rows=(20, 64, 256), steps=10):
+    """Action length K crossed with the prefill length, as in the paper's K experiment (a
+    prefill of 256 vision rows plus an instruction of 20, 64 or 256 token ids: L_P = 276, 320,
+    512): the 32-layer pipeline at each point (one L_P-row prefill + K - 1 decode rows per step,
+    ring K + 1 slots), against the plain per-request schedule on the same kernels (prefill,
+    then K - 1 single-row decodes)."""
     import torch
     import workload as wl
     from paper_2512_20276_amd.pipeline import Pipeline
-    L_P, D = int(pids.numel()), shape.d_model
-    L_V = int((pids < 0).sum().item())
+    D, L_V = shape.d_model, 256
     out = []
-    for K in Ks:
-        max_pos = (L_P + K + 31) // 32 * 32
-        ring = af.Ring(shape.n_layers, K + 1, max_pos, shape.n_heads, shape.head_dim, dtype=torch.bfloat16)
-        pool = []
-        for i in range(4):
-            e = torch.zeros((L_P + K - 1, D), dtype=torch.bfloat16, device="cuda")
-            e[:L_V] = wl.draw(("vision", 0, i), (L_V, D), device="cuda")
-            pool.append(e)
-        pipe = Pipeline(w, ring, K, pids, lambda t: pool[t % len(pool)], keep_history=False)
-        for _ in range(K + 1):
-            pipe.step()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(steps):
-            M = pipe.step().M
-        torch.cuda.synchronize()
-        dt = (time.perf_counter() - t0) / steps
-        ring.close()
-        seq_ms = sequential_baseline(af, w, shape, pids, pool, K, n_req=3, warm=1)
-        out.append({"K": K, "M": M, "ms_per_step": round(dt * 1e3, 3), "packed_steps_per_s": round(1 / dt, 2),
-                    "packed_tokens_per_s": round(M / dt, 1), "action_tokens_per_s": round(K / dt, 1),
-                    "sequential_ms_per_request": round(seq_ms, 3), "speedup_vs_sequential": round(seq_ms / (dt * 1e3), 3)})
-        log(f"K={K}: {dt * 1e3:.2f} ms/step, sequential {seq_ms:.2f} ms/request")
+    for L_T in text_rows:
+        text = wl.draw_ids(("instruction", 0, L_T), L_T, shape.vocab, device="cuda")
+        pids = torch.cat([torch.full((L_V,), -1, dtype=torch.int32, device="cuda"), text])
+        L_P = L_V + L_T
+        for K in Ks:
+            max_pos = (L_P + K + 31) // 32 * 32
+            ring = af.Ring(shape.n_layers, K + 1, max_pos, shape.n_heads, shape.head_dim, dtype=torch.bfloat16)
+            pool = []
+            for i in range(4):
+                e = torch.zeros((L_P + K - 1, D), dtype=torch.bfloat16, device="cuda")
+                e[:L_V] = wl.draw(("vision", 0, i), (L_V, D), device="cuda")
+                pool.append(e)
+            pipe = Pipeline(w, ring, K, pids, lambda t: pool[t % len(pool)], keep_history=False)
+            for _ in range(K + 1):
+                pipe.step()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(steps):
+                M = pipe.step().M
+            torch.cuda.synchronize()
+            dt = (time.perf_counter() - t0) / steps
+            ring.close()
+            seq_ms = sequential_baseline(af, w, shape, pids, pool, K, n_req=2, warm=1)
+            out.append({"K": K, "L_P": L_P, "M": M, "ms_per_step": round(dt * 1e3, 3),
+                        "packed_steps_per_s": round(1 / dt, 2), "packed_tokens_per_s": round(M / dt, 1),
+                        "action_tokens_per_s": round(K / dt, 1), "sequential_ms_per_request": round(seq_ms, 3),
+                        "speedup_vs_sequential": round(seq_ms / (dt * 1e3), 3)})
+            log(f"K={K} L_P={L_P}: {dt * 1e3:.2f} ms/step, sequential {seq_ms:.2f} ms/request")
     return out
 
 
@@ -536,53 +542,98 @@ def naive_pipe(af, w, shape, pids, pool, packed_ms, K=7, steps=12):
 
 
 # ----------------------------------------------------------------------------- cpu baseline
-def cpu_baseline(seconds_budget: float):
-    """The oracle (float64 NumPy, as it stands) on a bounded sample of the same workload: one
-    steady-state packed step (276 prefill rows + 6 decode rows, contexts 277..282) through as
-    many 7B-shape layers as fit the time budget (at least one), extrapolated to 32 layers plus
-    the final norm / LM head of the 7 emitting rows."""
+def cpu_baseline(n_big_steps: int = 2):
+    """The oracle as it stands (float64 NumPy with bf16 storage rounding, never tuned for speed)
+    on the host cores, on bounded samples of the workloads:
+      * config 1: the tiny fp32-storage decoder's packed step 2 of a K = 3 pipeline (32 + 1 + 1 rows);
+      * config 2: one 7B-shape layer at the 282-row packed step (276 prefill + 6 decode rows);
+      * config 3: n_big_steps whole 282-row packed steps through all 32 layers and the LM head of
+        the 7 emitting rows; the weights are drawn one layer at a time and streamed (host memory
+        holds one float64 layer), and each layer is applied to every step's rows before the next
+        layer is drawn, so only the oracle's own arithmetic is timed.
+    The headline value is packed tokens/s at the median config-3 step."""
     import numpy as np
     import torch
     import threadpoolctl
 
     import oracle
+    from oracle.pipeline import PipelineOracle
     import workload as wl
 
-    shape = wl.LLAMA7B
-    H, hd, D = shape.n_heads, shape.head_dim, shape.d_model
+    info = threadpoolctl.threadpool_info()
+    blas_threads = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
+    cores = len(os.sched_getaffinity(0))
     to64 = lambda t: t.detach().to("cpu", torch.float64).numpy()
-    layers = [{k: to64(v) for k, v in wl.layer_weights(shape, l, seed=0, device="cuda").items()} for l in range(2)]
+    out = {}
+
+    # config 1: the tiny decoder's step 2 (warm-up steps 0 and 1 untimed)
+    tiny = wl.TINY
+    g, ls = wl.model_weights(tiny, seed=0)
+    tmodel = oracle.OracleModel(tiny, {k: to64(v) for k, v in g.items()},
+                                [{k: to64(v) for k, v in lw.items()} for lw in ls], storage="f32")
+
+    def tiny_prefill(t):
+        ids = wl.draw_ids(("prompt", 0, t), 32, tiny.vocab).numpy().astype(np.int64)
+        return ids, np.zeros((32, tiny.d_model))
+
+    tpipe = PipelineOracle(tmodel, 3, 4, 64, tiny_prefill)
+    tpipe.step()
+    tpipe.step()
+    t0 = time.perf_counter()
+    st = tpipe.step()
+    t1 = time.perf_counter() - t0
+    out["config1_step"] = {"M": int(len(st["ids"])), "seconds": round(t1, 4),
+                           "tokens_per_s": round(len(st["ids"]) / t1, 1)}
+    log(f"cpu oracle: config 1 step {t1 * 1e3:.1f} ms")
+
+    # configs 2 and 3: 282-row packed steps of the 7B shape, layer by layer
+    shape = wl.LLAMA7B
+    H, hd, D, L = shape.n_heads, shape.head_dim, shape.d_model, shape.n_layers
     glob = {k: to64(v) for k, v in wl.global_weights(shape, seed=0, device="cuda").items()}
-    torch.cuda.empty_cache()
-    model = oracle.OracleModel(shape.with_layers(2), glob, layers, storage="bf16")
     rng = np.random.default_rng(0)
-    kv = oracle.OracleRingKV(2, 8, 288, H, hd)
     segs = [oracle.Segment(0, 276, 2, 0, 10)] + [oracle.Segment(276 + s - 1, 1, (2 - s) % 8, 276 + s - 1, 10 - s)
                                                  for s in range(1, 7)]
-    for i, sg in enumerate(segs):
-        sg.q_start = 0 if i == 0 else 276 + i - 1
-        if sg.pos0:
-            kv.k[:, sg.slot, :sg.pos0] = rng.standard_normal((2, sg.pos0, H, hd))
-            kv.v[:, sg.slot, :sg.pos0] = rng.standard_normal((2, sg.pos0, H, hd))
-    x = oracle.round_storage(rng.standard_normal((282, D)), "bf16")
-    info = threadpoolctl.threadpool_info()
-    threads = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
-    t_layers, n = 0.0, 0
-    h = x
-    while n < 32 and (n == 0 or t_layers < seconds_budget):
+    steps = []
+    for b in range(n_big_steps):
+        # one layer of ring history (N(0, 1), bf16 values), which every layer of the sample reads
+        kv = oracle.OracleRingKV(1, 8, 288, H, hd)
+        for sg in segs:
+            if sg.pos0:
+                kv.k[0, sg.slot, :sg.pos0] = oracle.round_storage(rng.standard_normal((sg.pos0, H, hd)), "bf16")
+                kv.v[0, sg.slot, :sg.pos0] = oracle.round_storage(rng.standard_normal((sg.pos0, H, hd)), "bf16")
+        x = oracle.round_storage(rng.standard_normal((282, D)), "bf16")
+        steps.append({"kv": kv, "h": x, "layer_s": []})
+    for l in range(L):
+        lw = {k: to64(v) for k, v in wl.layer_weights(shape, l, seed=0, device="cuda").items()}
+        model = oracle.OracleModel(shape.with_layers(1), glob, [lw], storage="bf16")
+        for stp in steps:
+            t0 = time.perf_counter()
+            stp["h"] = model.layer_packed(0, stp["h"], segs, stp["kv"])
+            stp["layer_s"].append(time.perf_counter() - t0)
+        del model, lw
+        if l % 8 == 7:
+            log(f"cpu oracle: {l + 1} of {L} layers of {n_big_steps} steps")
+    torch.cuda.empty_cache()
+    head_model = oracle.OracleModel(shape.with_layers(0), glob, [], storage="bf16")
+    step_s = []
+    for stp in steps:
         t0 = time.perf_counter()
-        h = model.layer_packed(n % 2, h, segs, kv)
-        t_layers += time.perf_counter() - t0
-        n += 1
-        log(f"cpu oracle: layer {n} done ({t_layers:.1f} s)")
-    t0 = time.perf_counter()
-    model.logits(h[[s.q_start + s.q_len - 1 for s in segs]])
-    t_head = time.perf_counter() - t0
-    step_s = t_layers / n * 32 + t_head
-    return {"value": 282.0 / step_s, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"one 282-row packed step through {n} of 32 layers ({t_layers:.1f} s) + LM head "
-                      f"({t_head:.2f} s), extrapolated to 32 layers: {step_s:.1f} s/step",
-            "seconds_per_step": step_s}
+        head_model.logits(stp["h"][[s.q_start + s.q_len - 1 for s in segs]])
+        step_s.append(sum(stp["layer_s"]) + time.perf_counter() - t0)
+    layer_s = sorted(t for stp in steps for t in stp["layer_s"])
+    q = lambda v, f: v[min(len(v) - 1, int(f * len(v)))]
+    out["config2_layer_step"] = {"M": 282, "median_s": round(q(layer_s, 0.5), 4), "p10_s": round(q(layer_s, 0.1), 4),
+                                 "p90_s": round(q(layer_s, 0.9), 4), "samples": len(layer_s)}
+    med = sorted(step_s)[len(step_s) // 2]
+    out["config3_steps"] = {"M": 282, "layers": L, "seconds": [round(t, 3) for t in step_s],
+                            "median_s": round(med, 3)}
+    log(f"cpu oracle: config 3 steps {[round(t, 2) for t in step_s]} s")
+    return {"value": round(282.0 / med, 2), "unit": "tokens/s", "cores": cores, "blas_threads": int(blas_threads),
+            "kind": "oracle", "precision": "float64 arithmetic, bf16 storage rounding (fp32 for config 1)",
+            "sample": f"{n_big_steps} whole 282-row packed steps of the 32-layer 7B shape (weights streamed a layer "
+                      f"at a time, LM head on 7 rows), median {med:.1f} s/step; plus one config-1 step and the "
+                      f"config-2 layer steps they contain",
+            **out}
 
 
 # ----------------------------------------------------------------------------- main
@@ -687,7 +738,8 @@ def main():
         mfma_frac = gemm_flops / (gemm_ms * 1e-3) / (PEAK_BF16_TFLOPS * 1e12)
         ga_ms, ga_n = tm["gemm_gateup"]
         ga_avg = ga_ms / ga_n
-        ga_flops, ga_bytes = work["gemm_gateup"]
+        ga_flops, _ = work["gemm_gateup"]
+        ga_bytes = 2 * (2 * F * D)   # algorithmic bytes: the gate and up weights, each read once
         ga_gbs = ga_bytes / (ga_avg * 1e-3) / 1e9
         at_ms, at_n = tm["attention"]
         at_bytes = attention_bytes(segs_seen, H, hd)
@@ -695,8 +747,11 @@ def main():
         out["roofline"] = {"kernel": "gemm32c_kernel<5, 6, EPI_SWIGLU> (gate/up projection, SwiGLU epilogue)",
                            "bound": "hbm", "achieved": round(ga_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                            "frac": round(ga_gbs / PEAK_HBM_GBS, 4), "traffic": measured_traffic(),
-                           "bytes_per_launch": ga_bytes, "avg_launch_us": round(ga_avg * 1e3, 2),
-                           "tflops": round(ga_flops / (ga_avg * 1e-3) / 1e12, 1)}
+                           "bytes_per_launch": ga_bytes, "bytes_counted": "gate + up weights (2 x 11008 x 4096 bf16)",
+                           "avg_launch_us": round(ga_avg * 1e3, 2),
+                           "duration": f"average of {ga_n} launches, HIP events on the launch stream (timing pass)",
+                           "tflops": round(ga_flops / (ga_avg * 1e-3) / 1e12, 1),
+                           "frac_mfma": round(ga_flops / (ga_avg * 1e-3) / (PEAK_BF16_TFLOPS * 1e12), 4)}
         out["mfma_frac_projection_gemms"] = round(mfma_frac, 4)
         out["projection_gemm_tflops"] = round(gemm_flops / (gemm_ms * 1e-3) / 1e12, 1)
         out["attention_hbm"] = {"GB/s": round(at_gbs, 1), "frac": round(at_gbs / PEAK_HBM_GBS, 4),
@@ -705,6 +760,19 @@ def main():
         out["kernel_sum_ms_per_step"] = round(sum(ms for ms, _ in tm.values()) / args.steps, 4)
         out["timing_pass_ms_per_step"] = round(t_inst / args.steps * 1e3, 4)
         log(f"timing pass: {json.dumps(per_step)}")
+
+        # per-step GPU time: an event pair around every step on the launch stream, no host waits
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+        for a, b in evs:
+            a.record()
+            pipe.step()
+            b.record()
+        torch.cuda.synchronize()
+        st_ms = sorted(a.elapsed_time(b) for a, b in evs)
+        q = lambda f: st_ms[min(len(st_ms) - 1, int(f * len(st_ms)))]
+        out["step_ms_distribution"] = {"median": round(q(0.5), 4), "p10": round(q(0.1), 4), "p90": round(q(0.9), 4),
+                                       "steps": len(st_ms), "how": "HIP events around each step, no host waits"}
 
     extras = () if args.no_extra else tuple(args.extra or EXTRAS)
     if "sequential" in extras:
@@ -725,8 +793,8 @@ def main():
         log("stress workload (8 pipelines, M = 2264, 32 layers)")
         out["stress"] = stress(af, w, shape)
     if "k_sweep" in extras:
-        log("K sweep (K = 7, 16, 24, 32)")
-        out["k_sweep"] = k_sweep(af, w, shape, pids)
+        log("K sweep (K = 7, 16, 24, 32 x prefill 276, 320, 512)")
+        out["k_sweep"] = k_sweep(af, w, shape)
     if "copy_shift" in extras:
         log("physical-copy stage shift (the paper's InPlaceKVShift copy) against the rotation")
         out["copy_shift"] = copy_shift(af, w, shape, pids, pool, K)
@@ -738,7 +806,7 @@ def main():
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle sample)")
-        out["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(args.cpu_steps)
     print(json.dumps(out), flush=True)
 
 

@@ -13,7 +13,7 @@ CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libactionflow.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 
-HIP_SOURCES = ["af_kernels.hip", "af_noalloc.hip"]
+HIP_SOURCES = ["af_gemm.hip", "af_attention.hip", "af_kernels.hip", "af_noalloc.hip"]
 HOST_SOURCES = ["af_ring.cpp", "af_model.cpp"]
 
 # Packed-fp32 instructions are disabled for all device code (hipcc makes them from plain float
@@ -37,20 +37,33 @@ def _run(cmd):
     return out
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source and link the shared library; returns its path."""
+HEADERS = [os.path.join(CSRC, "af_internal.h"), os.path.join(CSRC, "af_device.h"),
+           os.path.join(ROOT, "include", "actionflow.h")]
+
+
+def _stale(src: str, obj: str) -> bool:
+    if not os.path.exists(obj):
+        return True
+    t = os.path.getmtime(obj)
+    return any(os.path.getmtime(p) > t for p in [src, *HEADERS])
+
+
+def build(verbose: bool = False, changed_only: bool = False) -> str:
+    """Compile every source (with changed_only: those newer than their object or than a header)
+    and link the shared library; returns its path."""
     cc = hipcc()
     os.makedirs(BUILD_DIR, exist_ok=True)
-    jobs = []
-    for src in HIP_SOURCES:
-        obj = os.path.join(BUILD_DIR, src + ".o")
-        jobs.append([cc, *COMMON, *DEVICE_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
-    for src in HOST_SOURCES:
-        obj = os.path.join(BUILD_DIR, src + ".o")
-        jobs.append([cc, *COMMON, "-c", os.path.join(CSRC, src), "-o", obj])
-    with ThreadPoolExecutor(max_workers=len(jobs)) as ex:
-        logs = list(ex.map(_run, jobs))
-    objs = [j[-1] for j in jobs]
+    jobs, objs = [], []
+    for srcs, flags in ((HIP_SOURCES, DEVICE_FLAGS), (HOST_SOURCES, [])):
+        for src in srcs:
+            path, obj = os.path.join(CSRC, src), os.path.join(BUILD_DIR, src + ".o")
+            objs.append(obj)
+            if not changed_only or _stale(path, obj):
+                jobs.append([cc, *COMMON, *flags, "-c", path, "-o", obj])
+    logs = []
+    if jobs:
+        with ThreadPoolExecutor(max_workers=len(jobs)) as ex:
+            logs = list(ex.map(_run, jobs))
     tmp = OUT + ".tmp"
     logs.append(_run([cc, "-shared", "-fPIC", *DEVICE_FLAGS, *objs, "-o", tmp]))
     os.replace(tmp, OUT)
@@ -62,4 +75,4 @@ def build(verbose: bool = False) -> str:
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, changed_only="--changed" in sys.argv))

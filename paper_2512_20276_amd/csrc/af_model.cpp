@@ -1,7 +1,8 @@
 // Weights, scratch activations and the orchestration of the packed forward (Alg. 1 head,
 // Alg. 2 per layer).  Host code only: argument checking, the per-call step descriptor
 // (segment table, per-row slot/position, attention work tiles, emitting rows) and the
-// kernel sequence.  Every step of the path runs in the kernels of af_kernels.hip.
+// kernel sequence.  Every step of the path runs in the kernels of af_gemm.hip, af_attention.hip
+// and af_kernels.hip.
 #include <algorithm>
 #include <cmath>
 #include <cstring>

@@ -38,11 +38,11 @@ def _weights(shape, device="cuda", random_gains=False):
 
 
 # ----------------------------------------------------------------------------- tiny fp32 pipeline
-@pytest.mark.parametrize("K", [3, 8])
+@pytest.mark.parametrize("K", [3, 8, 16])
 def test_tiny_fp32_pipeline_matches_oracle(K):
     """K = 3 is the tiny configuration (step 2 packs 32 + 1 + 1 = 34 rows); K = 8 packs seven
     decode rows beside each prefill (an odd number: the last pair of decode rows is half idle)
-    and wraps a 9-slot ring."""
+    and wraps a 9-slot ring; K = 16 (the K sweep's second point) packs fifteen and wraps 17."""
     shape = wl.TINY
     L_P = 32
     n_slots, max_pos = (4, 64) if K == 3 else (K + 1, L_P + K)
@@ -446,13 +446,15 @@ def test_7b_32_layer_packed_equals_sequential_on_gpu(split_k):
 
 
 @pytest.mark.timeout(600)
-def test_7b_k32_packed_equals_sequential_4_layers():
-    """The largest K of the K sweep (K = 32: a 276-row prefill packed with 31 decode rows, M =
-    307, whose decode rows take their own attention launch): with split-K off every row, logit
-    and token of requests 0 and 1 equals the plain per-request run on the same kernels, bit for
-    bit (a 4-layer model of the 7B shape)."""
+@pytest.mark.parametrize("K,L_T", [(16, 20), (24, 64), (32, 20)])
+def test_7b_k_sweep_packed_equals_sequential_4_layers(K, L_T):
+    """The K sweep's points beyond K = 7 (a prefill of 256 vision rows and L_T instruction rows
+    packed with K - 1 decode rows; at K = 24 and 32 the decode rows take their own attention
+    launch; K = 24 with the 64-row instruction of a longer prefill): with split-K off every row,
+    logit and token of requests 0 and 1 equals the plain per-request run on the same kernels,
+    bit for bit (a 4-layer model of the 7B shape)."""
     shape = wl.LLAMA7B.with_layers(4)
-    K, L_V, L_T = 32, 256, 20
+    L_V = 256
     L_P, D, V = L_V + L_T, shape.d_model, shape.vocab
     g, layers, w = _weights(shape)
     del g, layers
@@ -478,7 +480,7 @@ def test_7b_k32_packed_equals_sequential_4_layers():
             if sg[4] in rows:
                 rows[sg[4]][sg[3]] = to_np(res.hidden[sg[0]:sg[0] + sg[1]])
                 logits[sg[4]][sg[3]] = to_np(res.logits[j])
-    assert max(Ms) == L_P + K - 1 == 307
+    assert max(Ms) == L_P + K - 1
     packed_tokens = {r: pipe.request_tokens(r) for r in rows}
     ring.close()
     for r in rows:
