@@ -39,13 +39,13 @@ __device__ __forceinline__ float dot_vec(const uint4& k, const uint4& q, float a
   }
 }
 
-// ROWS (1 or 2) single-row segments per workgroup: tiles first .. first + ROWS - 1 (those that
-// exist), each on ATTN_WAVES / ROWS waves.  Two per workgroup halve the workgroups a packed
+// ROWS (1 or 2) single-row segments per workgroup of NWG waves: tiles first .. first + ROWS - 1
+// (those that exist), each on NWG / ROWS waves.  Two per workgroup halve the workgroups a packed
 // step's decode rows take next to its query tiles.  Either way a row is computed as ATTN_WAVES
-// virtual waves (virtual wave v takes chunks v, v + ATTN_WAVES, ..; a wave of a pair runs two
-// of them one after the other) merged in virtual-wave order, so the result does not depend on
-// how many rows share the workgroup.
-template <typename T, int HD, int ROWS>
+// virtual waves (virtual wave v takes chunks v, v + ATTN_WAVES, ..; a wave of a row on four
+// waves runs two of them one after the other) merged in virtual-wave order, so the result does
+// not depend on how many rows share the workgroup or how many waves it has.
+template <typename T, int HD, int ROWS, int NWG = ATTN_WAVES>
 __device__ __forceinline__ void attention_decode_rows(const AttnArgs& a, int first) {
   constexpr int VEC = Chunk<T>::N;  // elements per 16 bytes
   constexpr int DG = HD / VEC;      // 16-byte chunks per key row
@@ -54,8 +54,9 @@ __device__ __forceinline__ void attention_decode_rows(const AttnArgs& a, int fir
   constexpr int KPL = 32 / KG;      // values: keys per lane per 32-key chunk
   static_assert(DG % 2 == 0 && DG <= 64 && 64 % DG == 0 && 32 % KG == 0, "head_dim");
   static_assert(ROWS == 1 || ROWS == 2, "rows per workgroup");
-  constexpr int VW = ATTN_WAVES;         // virtual waves per row
-  constexpr int NW = ATTN_WAVES / ROWS;  // waves per row
+  constexpr int VW = ATTN_WAVES;  // virtual waves per row
+  constexpr int NW = NWG / ROWS;  // waves per row
+  static_assert(VW % NW == 0, "virtual waves per wave");
   __shared__ float wm[ROWS][VW], wl[ROWS][VW];
   __shared__ __attribute__((aligned(16))) float wo[ROWS][VW][HD];
   __shared__ __attribute__((aligned(16))) uint4 qs[ROWS][DG];
@@ -160,25 +161,50 @@ __device__ __forceinline__ void attention_decode_rows(const AttnArgs& a, int fir
 
 // Query tiles of multi-row segments.  The next key/value tile is loaded into registers while
 // the current one is processed from LDS (one memory latency per segment, not per tile).
+// The segment's key tiles are split between two key groups (group g takes tiles g, g + 2,
+// g + 4, ..), each with a softmax state of its own, and group 1's state is merged into group
+// 0's at the end.  With NWG = 8 waves the two groups run at once, four waves each, with LDS
+// buffers of their own; with NWG = 4 one set of waves runs group 0 and then group 1, parking
+// group 0's state in LDS.  Both do the same arithmetic in the same order, so a row's result
+// does not depend on which of the two ran it.
 template <typename T, int HD>
-__device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int tile) {
-  constexpr int VEC = Chunk<T>::N;
-  constexpr int KROW = HD + VEC;            // padded key row (elements)
-  constexpr int VROW = ATTN_BKV + VEC;      // padded transposed-value row
+struct AttnLds {
+  static constexpr int VEC = Chunk<T>::N;
+  static constexpr int KROW = HD + VEC;        // padded key row (elements)
+  static constexpr int VROW = ATTN_BKV + VEC;  // padded transposed-value row
+  static constexpr int K_ELEMS = ATTN_BKV * KROW, V_ELEMS = HD * VROW;
+  static constexpr int GROUP_BYTES = (K_ELEMS + V_ELEMS) * (int)sizeof(T);
+  static constexpr int MERGE_BYTES = 4 * 64 * (2 + 4 * (HD / 16)) * (int)sizeof(float);  // 4 waves' states
+  // LDS of a query-tile workgroup: two groups' buffers (8 waves; the merge reuses them), or one
+  // group's buffers and the parked state (4 waves)
+  static constexpr int bytes(int nwg) { return nwg == 8 ? 2 * GROUP_BYTES : GROUP_BYTES + MERGE_BYTES; }
+};
+
+// The merge of key group 1's state (m1, l1, o1) into group 0's (m0, l0, o0).
+__device__ __forceinline__ void merge_state(float& m0, float& l0, float m1, float l1, float& f0, float& f1) {
+  const float M = fmaxf(m0, m1);
+  f0 = m0 == -INFINITY ? 0.f : exp2f(m0 - M);
+  f1 = m1 == -INFINITY ? 0.f : exp2f(m1 - M);
+  l0 = __builtin_fmaf(l0, f0, l1 * f1);
+  m0 = M;
+}
+
+template <typename T, int HD, int NWG>
+__device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int tile, char* smem) {
+  typedef AttnLds<T, HD> L;
+  constexpr int VEC = L::VEC, KROW = L::KROW, VROW = L::VROW;
   constexpr int KST = HD / 32;              // MFMA k steps over the head dimension
   constexpr int DB = HD / 16;               // 16-dim output blocks
   constexpr int CPR = HD / VEC;             // 16-byte chunks per key row
   constexpr int NCH = ATTN_BKV * CPR / 256; // chunks of K (and of V) per thread per tile
-  static_assert((ATTN_BKV * CPR) % 256 == 0, "tile shape");
+  constexpr int NPG = NWG / 4;              // key groups running at once
+  static_assert((ATTN_BKV * CPR) % 256 == 0 && (NWG == 4 || NWG == 8), "tile shape");
   typedef typename Mma<T>::frag frag;
 
-  // two key groups of four waves: group g takes key tiles g, g + 2, g + 4, .. of the segment
-  // with buffers of its own; the groups' partial softmax states are merged at the end
-  __shared__ __attribute__((aligned(16))) T Ks[2][ATTN_BKV * KROW];
-  __shared__ __attribute__((aligned(16))) T Vt[2][HD * VROW];
-
-  const int lane = threadIdx.x & 63, grp = threadIdx.x >> 8, wave = (threadIdx.x >> 6) & 3;
+  const int lane = threadIdx.x & 63, pgrp = threadIdx.x >> 8, wave = (threadIdx.x >> 6) & 3;
   const int tid = threadIdx.x & 255;  // position within the key group
+  T* const Ks = (T*)smem + (size_t)pgrp * (L::K_ELEMS + L::V_ELEMS);
+  T* const Vt = Ks + L::K_ELEMS;
   const int lr = lane & 15, lg = lane >> 4;
   const int seg_i = a.tiles[2 * tile], i0 = a.tiles[2 * tile + 1];
   const int h = blockIdx.y;
@@ -204,10 +230,6 @@ __device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int ti
     for (int s = 0; s < KST; ++s) qf[s] = *(const frag*)(qrow + s * 32 + lg * 8);
   }
 
-  f32x4 oacc[DB];
-#pragma unroll
-  for (int d = 0; d < DB; ++d) oacc[d] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY, l_run = 0.f;
 
   // One tile's keys and values in registers.  Keys: thread t holds 16-byte chunk t % CPR of
   // keys t / CPR + KR j (row-major LDS writes, one key row per CPR lanes).  Values: thread t
@@ -231,143 +253,167 @@ __device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int ti
   };
   const int n_kt = (kv_end + ATTN_BKV - 1) / ATTN_BKV;
   const int n_it = (n_kt + 1) / 2;  // both groups run the same iterations (and barriers)
-  load_tile(grp * ATTN_BKV);        // keys past kv_end load as zeros
-  for (int it = 0; it < n_it; ++it) {
-    const int kt = 2 * it + grp;
-    const int kb0 = kt * ATTN_BKV;
-    // ---- park the tile in LDS: keys row-major, values transposed
-    __syncthreads();  // the previous tile's LDS reads are done
+  f32x4 oacc[DB];
+  float m_run = -INFINITY, l_run = 0.f;
+  float* const park = (float*)(smem + L::GROUP_BYTES) + (size_t)wave * (2 + 4 * DB) * 64 + lane;
+  for (int grp = pgrp; grp < 2; grp += NPG) {
 #pragma unroll
-    for (int j = 0; j < NCH; ++j) *(uint4*)(&Ks[grp][(kr + KR * j) * KROW + kc * VEC]) = kreg[j];
-    {
-      T vt[NCH][VEC];
+    for (int d = 0; d < DB; ++d) oacc[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+    m_run = -INFINITY;
+    l_run = 0.f;
+    load_tile(grp * ATTN_BKV);        // keys past kv_end load as zeros
+    for (int it = 0; it < n_it; ++it) {
+      const int kt = 2 * it + grp;
+      const int kb0 = kt * ATTN_BKV;
+      // ---- park the tile in LDS: keys row-major, values transposed
+      __syncthreads();  // the previous tile's LDS reads are done
 #pragma unroll
-      for (int j = 0; j < NCH; ++j) __builtin_memcpy(vt[j], &vreg[j], 16);
+      for (int j = 0; j < NCH; ++j) *(uint4*)(&Ks[(kr + KR * j) * KROW + kc * VEC]) = kreg[j];
+      {
+        T vt[NCH][VEC];
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) {
-        T col[KPT];
+        for (int j = 0; j < NCH; ++j) __builtin_memcpy(vt[j], &vreg[j], 16);
 #pragma unroll
-        for (int j = 0; j < KPT; ++j) col[j] = vt[j][e];
-        T* dst = &Vt[grp][(vc * VEC + e) * VROW + vg * KPT];
-        if constexpr (KPT * sizeof(T) == 4) {
-          *(unsigned*)dst = *(const unsigned*)col;
-        } else if constexpr (KPT * sizeof(T) == 8) {
-          *(uint2*)dst = *(const uint2*)col;
-        } else {
-          static_assert((KPT * sizeof(T)) % 16 == 0, "value chunk");
+        for (int e = 0; e < VEC; ++e) {
+          T col[KPT];
 #pragma unroll
-          for (int q = 0; q < (int)(KPT * sizeof(T)) / 16; ++q) *(uint4*)(dst + q * 16 / sizeof(T)) = *(const uint4*)(col + q * 16 / sizeof(T));
+          for (int j = 0; j < KPT; ++j) col[j] = vt[j][e];
+          T* dst = &Vt[(vc * VEC + e) * VROW + vg * KPT];
+          if constexpr (KPT * sizeof(T) == 4) {
+            *(unsigned*)dst = *(const unsigned*)col;
+          } else if constexpr (KPT * sizeof(T) == 8) {
+            *(uint2*)dst = *(const uint2*)col;
+          } else {
+            static_assert((KPT * sizeof(T)) % 16 == 0, "value chunk");
+#pragma unroll
+            for (int q = 0; q < (int)(KPT * sizeof(T)) / 16; ++q) *(uint4*)(dst + q * 16 / sizeof(T)) = *(const uint4*)(col + q * 16 / sizeof(T));
+          }
+        }
+      }
+      __syncthreads();
+      if (kt + 2 < n_kt) load_tile(kb0 + 2 * ATTN_BKV);  // this group's next tile, in flight meanwhile
+
+      if (wave_rows > 0 && kb0 <= wave_last_pos) {
+        // ---- S^T = K . Q^T for 4 blocks of 16 keys
+        float p[4][4];
+        float tmax = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+          f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int s = 0; s < KST; ++s) {
+            const frag kf = *(const frag*)(&Ks[(kb * 16 + lr) * KROW + s * 32 + lg * 8]);
+            sacc = Mma<T>::mma(kf, qf[s], sacc);
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int key = kb0 + kb * 16 + lg * 4 + e;
+            const float v = key <= qpos ? sacc[e] * a.scale_log2 : -INFINITY;
+            p[kb][e] = v;
+            tmax = fmaxf(tmax, v);
+          }
+        }
+        tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
+        tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+        const float m_new = fmaxf(m_run, tmax);
+        // a row may not have seen any key yet (key group 1's first tile can lie wholly past some
+        // rows): then every score so far is -inf, and 0 stands in as the reference so that the
+        // probabilities and the correction come out 0 instead of exp2(-inf - -inf)
+        const float m_ref = m_new == -INFINITY ? 0.f : m_new;
+        const float corr = exp2f(m_run - m_ref);  // m_run = -inf before the row's first key -> 0
+        float psum = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float pe = exp2f(p[kb][e] - m_ref);
+            p[kb][e] = pe;
+            psum += pe;
+          }
+        l_run = l_run * corr + psum;
+        m_run = m_new;
+#pragma unroll
+        for (int d = 0; d < DB; ++d) oacc[d] *= corr;
+        // ---- O^T += V^T . P^T over two 32-key chunks.  In bf16 the probabilities are split
+        // into a bf16 head and a bf16 remainder (two MFMAs), so P keeps ~16 significant bits and
+        // the product is as accurate as an fp32 one; V is exact in bf16.
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          frag pf, pf_lo;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float pv = e < 4 ? p[2 * c][e] : p[2 * c + 1][e - 4];
+            pf[e] = from_f<T>(pv);
+            pf_lo[e] = from_f<T>(pv - to_f(pf[e]));
+          }
+#pragma unroll
+          for (int d = 0; d < DB; ++d) {
+            // keys lg * 4 .. +3 and 16 + lg * 4 .. +3 of the chunk: two aligned 4-element reads
+            const T* vrow = &Vt[(d * 16 + lr) * VROW + c * 32 + lg * 4];
+            frag vf;
+            if constexpr (sizeof(T) == 2) {
+              typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4_;
+              const bf16x4_ lo = *(const bf16x4_*)vrow, hi = *(const bf16x4_*)(vrow + 16);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                vf[e] = lo[e];
+                vf[4 + e] = hi[e];
+              }
+            } else {
+              const f32x4 lo = *(const f32x4*)vrow, hi = *(const f32x4*)(vrow + 16);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                vf[e] = lo[e];
+                vf[4 + e] = hi[e];
+              }
+            }
+            oacc[d] = Mma<T>::mma(vf, pf, oacc[d]);
+            if constexpr (sizeof(T) == 2) oacc[d] = Mma<T>::mma(vf, pf_lo, oacc[d]);
+          }
         }
       }
     }
-    __syncthreads();
-    if (kt + 2 < n_kt) load_tile(kb0 + 2 * ATTN_BKV);  // this group's next tile, in flight meanwhile
-
-    if (wave_rows > 0 && kb0 <= wave_last_pos) {
-      // ---- S^T = K . Q^T for 4 blocks of 16 keys
-      float p[4][4];
-      float tmax = -INFINITY;
+    if (NWG == 4 && grp == 0) {  // park group 0's state for the merge
+      park[0] = m_run;
+      park[64] = l_run;
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int d = 0; d < DB; ++d)
 #pragma unroll
-        for (int s = 0; s < KST; ++s) {
-          const frag kf = *(const frag*)(&Ks[grp][(kb * 16 + lr) * KROW + s * 32 + lg * 8]);
-          sacc = Mma<T>::mma(kf, qf[s], sacc);
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int key = kb0 + kb * 16 + lg * 4 + e;
-          const float v = key <= qpos ? sacc[e] * a.scale_log2 : -INFINITY;
-          p[kb][e] = v;
-          tmax = fmaxf(tmax, v);
-        }
-      }
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-      const float m_new = fmaxf(m_run, tmax);
-      // a row may not have seen any key yet (key group 1's first tile can lie wholly past some
-      // rows): then every score so far is -inf, and 0 stands in as the reference so that the
-      // probabilities and the correction come out 0 instead of exp2(-inf - -inf)
-      const float m_ref = m_new == -INFINITY ? 0.f : m_new;
-      const float corr = exp2f(m_run - m_ref);  // m_run = -inf before the row's first key -> 0
-      float psum = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float pe = exp2f(p[kb][e] - m_ref);
-          p[kb][e] = pe;
-          psum += pe;
-        }
-      l_run = l_run * corr + psum;
-      m_run = m_new;
-#pragma unroll
-      for (int d = 0; d < DB; ++d) oacc[d] *= corr;
-      // ---- O^T += V^T . P^T over two 32-key chunks.  In bf16 the probabilities are split
-      // into a bf16 head and a bf16 remainder (two MFMAs), so P keeps ~16 significant bits and
-      // the product is as accurate as an fp32 one; V is exact in bf16.
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        frag pf, pf_lo;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float pv = e < 4 ? p[2 * c][e] : p[2 * c + 1][e - 4];
-          pf[e] = from_f<T>(pv);
-          pf_lo[e] = from_f<T>(pv - to_f(pf[e]));
-        }
-#pragma unroll
-        for (int d = 0; d < DB; ++d) {
-          // keys lg * 4 .. +3 and 16 + lg * 4 .. +3 of the chunk: two aligned 4-element reads
-          const T* vrow = &Vt[grp][(d * 16 + lr) * VROW + c * 32 + lg * 4];
-          frag vf;
-          if constexpr (sizeof(T) == 2) {
-            typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4_;
-            const bf16x4_ lo = *(const bf16x4_*)vrow, hi = *(const bf16x4_*)(vrow + 16);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              vf[e] = lo[e];
-              vf[4 + e] = hi[e];
-            }
-          } else {
-            const f32x4 lo = *(const f32x4*)vrow, hi = *(const f32x4*)(vrow + 16);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              vf[e] = lo[e];
-              vf[4 + e] = hi[e];
-            }
-          }
-          oacc[d] = Mma<T>::mma(vf, pf, oacc[d]);
-          if constexpr (sizeof(T) == 2) oacc[d] = Mma<T>::mma(vf, pf_lo, oacc[d]);
-        }
-      }
+        for (int e = 0; e < 4; ++e) park[(2 + 4 * d + e) * 64] = oacc[d][e];
     }
   }
 
   // ---- merge key group 1 into group 0 (per lane: the same query and output dims in both)
   constexpr int NF = 2 + 4 * DB;  // m, l, the output accumulators
-  static_assert(4 * 64 * NF * sizeof(float) <= sizeof(Ks), "merge buffer");
-  float* mb = (float*)&Ks[0][0] + (size_t)wave * NF * 64 + lane;
-  __syncthreads();  // every wave is done with the key/value buffers
-  if (grp == 1) {
-    mb[0] = m_run;
-    mb[64] = l_run;
+  static_assert(4 * 64 * NF * sizeof(float) <= (size_t)L::GROUP_BYTES && 4 * 64 * NF * sizeof(float) <= (size_t)L::MERGE_BYTES,
+                "merge buffer");
+  if constexpr (NWG == 8) {
+    float* mb = (float*)smem + (size_t)wave * NF * 64 + lane;
+    __syncthreads();  // every wave is done with the key/value buffers
+    if (pgrp == 1) {
+      mb[0] = m_run;
+      mb[64] = l_run;
+#pragma unroll
+      for (int d = 0; d < DB; ++d)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) mb[(2 + 4 * d + e) * 64] = oacc[d][e];
+    }
+    __syncthreads();
+    if (pgrp == 1) return;
+    float f0, f1;
+    merge_state(m_run, l_run, mb[0], mb[64], f0, f1);
 #pragma unroll
     for (int d = 0; d < DB; ++d)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) mb[(2 + 4 * d + e) * 64] = oacc[d][e];
-  }
-  __syncthreads();
-  if (grp == 1) return;
-  {
-    const float m1 = mb[0], l1 = mb[64];
-    const float M = fmaxf(m_run, m1);
-    const float f0 = m_run == -INFINITY ? 0.f : exp2f(m_run - M), f1 = m1 == -INFINITY ? 0.f : exp2f(m1 - M);
-    l_run = l_run * f0 + l1 * f1;
+      for (int e = 0; e < 4; ++e) oacc[d][e] = __builtin_fmaf(oacc[d][e], f0, mb[(2 + 4 * d + e) * 64] * f1);
+  } else {  // this lane's state is group 1's; group 0's is parked
+    float m0 = park[0], l0 = park[64], f0, f1;
+    merge_state(m0, l0, m_run, l_run, f0, f1);
+    l_run = l0;
 #pragma unroll
     for (int d = 0; d < DB; ++d)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) oacc[d][e] = oacc[d][e] * f0 + mb[(2 + 4 * d + e) * 64] * f1;
+      for (int e = 0; e < 4; ++e) oacc[d][e] = __builtin_fmaf(park[(2 + 4 * d + e) * 64], f0, oacc[d][e] * f1);
   }
   if (wave_rows <= 0 || !q_ok) return;
   float l_tot = l_run + __shfl_xor(l_run, 16);
@@ -399,8 +445,9 @@ template <typename T, int HD, bool PREFILL>
 __global__ __launch_bounds__(64 * ATTN_WAVES, !PREFILL ? 4 : 2) void attention_kernel(AttnArgs a) {
   const int b = blockIdx.x;
   if constexpr (PREFILL) {
+    __shared__ __attribute__((aligned(16))) char smem[AttnLds<T, HD>::bytes(8)];
     if (b < a.n_multi)
-      attention_prefill_tile<T, HD>(a, b);
+      attention_prefill_tile<T, HD, 8>(a, b, smem);
     else
       attention_decode_rows<T, HD, 2>(a, a.n_multi + 2 * (b - a.n_multi));
   } else {
@@ -408,9 +455,27 @@ __global__ __launch_bounds__(64 * ATTN_WAVES, !PREFILL ? 4 : 2) void attention_k
   }
 }
 
-// Query tiles and decode rows share one launch, query tiles first; the decode-only kernel has
-// no query-tile LDS and registers and so fits more workgroups per CU, which pays once the decode
-// rows alone would more than fill the GPU twice over (a second launch then costs less).
+// Four-wave workgroups for steps whose decode rows would more than fill the GPU beside the query
+// tiles (many pipelines, long action chunks): block b < n_multi takes query tile b
+// (its key groups one after the other), any other block the single-row tile b.  Several such
+// workgroups share a CU, so the decode rows' key and value streams overlap the query tiles'
+// work; the results are those of the eight-wave instances bit for bit.
+template <typename T, int HD>
+__global__ __launch_bounds__(256, 3) void attention_kernel4(AttnArgs a) {
+  const int b = blockIdx.x;
+  __shared__ __attribute__((aligned(16))) char smem[AttnLds<T, HD>::bytes(4)];
+  if (b < a.n_multi)
+    attention_prefill_tile<T, HD, 4>(a, b, smem);
+  else
+    attention_decode_rows<T, HD, 1, 4>(a, b);
+}
+
+// Query tiles and decode rows share one launch, query tiles first: eight-wave workgroups (two
+// decode rows each) while the decode rows fit one pass over the CUs, else four-wave workgroups
+// (one decode row each), two of which share a CU; a step without query tiles takes the
+// decode-only instance.  Where the decode rows are many, overlapping their key and value
+// streams with the query tiles pays more than the query tiles' own two concurrent key groups
+// (measured on the 8-pipeline step); where they are few, the query tiles' latency decides.
 template <typename T, int HD>
 static void attention_launch(const AttnArgs& a0, int n_tiles, hipStream_t s) {
   AttnArgs a = a0;
@@ -422,9 +487,7 @@ static void attention_launch(const AttnArgs& a0, int n_tiles, hipStream_t s) {
   } else if ((long)n_pairs * a.n_heads <= 256) {
     hipLaunchKernelGGL((attention_kernel<T, HD, true>), dim3(a.n_multi + n_pairs, a.n_heads), block, 0, s, a);
   } else {
-    hipLaunchKernelGGL((attention_kernel<T, HD, true>), dim3(a.n_multi, a.n_heads), block, 0, s, a);
-    if (n_single > 0)  // the decode-only instance: its blocks start at the first single-row tile
-      hipLaunchKernelGGL((attention_kernel<T, HD, false>), dim3(n_single, a.n_heads), block, 0, s, a);
+    hipLaunchKernelGGL((attention_kernel4<T, HD>), dim3(n_tiles, a.n_heads), dim3(256), 0, s, a);
   }
 }
 
