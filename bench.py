@@ -62,6 +62,10 @@ def parse():
                         "SQ_VALU_MFMA_BUSY_CYCLES run and a --kernel-trace --stats run of the same command, and exit")
     p.add_argument("--summarize-stats", metavar="KERNEL_STATS_CSV",
                    help="print a per-kernel table of a rocprofv3 --kernel-trace --stats kernel_stats.csv and exit")
+    p.add_argument("--summarize-stalls", nargs=4, metavar=("SQ_CSV", "LDS_CSV", "TCP_CSV", "KERNEL_STATS_CSV"),
+                   help="print wait, MFMA, LDS and L1/L2 request figures per kernel class from three rocprofv3 "
+                        "--pmc runs (the counter sets of the profiling recipe) and a --kernel-trace --stats run, "
+                        "and exit")
     return p.parse_args()
 
 
@@ -157,7 +161,10 @@ def summarize_pmc(fetch_csv, write_csv):
         for r in csv.DictReader(open(path)):
             if r["Counter_Name"] != counter or "attention_kernel" not in r["Kernel_Name"]:
                 continue
-            inst = "decode-only" if "Lb0E" in r["Kernel_Name"] else "query tiles + decode rows"
+            name = r["Kernel_Name"]
+            inst = ("decode-only" if "Lb0E" in name else
+                    "four-wave: query tiles + decode rows" if "attention_kernel4" in name else
+                    "eight-wave: query tiles + decode-row pairs")
             a = acc[(inst, int(r["Grid_Size"]), int(r["Workgroup_Size"]))]
             a[0] += float(r["Counter_Value"])
             a[1] += 1
@@ -208,6 +215,46 @@ def summarize_mfma(counter_csv, stats_csv):
         us = dur[k][0] / dur[k][1] / 1e3 if dur[k][1] else float("nan")
         print(f"| {k} | {n} | {fl / 1e9:.3f} | {bc:.4g} | {us:.2f} | {fl / (us * 1e-6) / 1e12:.1f} | "
               f"{bc / (us * 1e-6 * 2.4e9 * 256 * 4):.4f} |")
+
+
+def summarize_stalls(sq_csv, lds_csv, tcp_csv, stats_csv):
+    """Where the waves of each kernel class spend their time, and the L1's outstanding L2 reads.
+    Counters (averaged per dispatch, summed over the chip): SQ_WAVE_CYCLES, SQ_WAIT_ANY,
+    SQ_WAIT_INST_ANY, SQ_WAIT_INST_LDS, SQ_VALU_MFMA_BUSY_CYCLES; SQ_INSTS_LDS, SQ_LDS_BANK_CONFLICT;
+    TCP_TCC_READ_REQ_sum (128-byte L2 reads), TCP_TCC_READ_REQ_LATENCY_sum (their summed latency,
+    cycles), TCP_PENDING_STALL_CYCLES_sum.  Reads in flight per CU = summed latency / (duration x
+    2.4 GHz x 256 CUs): by Little's law the number of L2 reads each CU keeps outstanding."""
+    import csv
+    from collections import defaultdict
+    acc = defaultdict(lambda: defaultdict(lambda: [0.0, 0]))
+    for path in (sq_csv, lds_csv, tcp_csv):
+        for r in csv.DictReader(open(path)):
+            a = acc[_kernel_class(r["Kernel_Name"])][r["Counter_Name"]]
+            a[0] += float(r["Counter_Value"])
+            a[1] += 1
+    dur = defaultdict(lambda: [0.0, 0])
+    for r in csv.DictReader(open(stats_csv)):
+        d = dur[_kernel_class(r["Name"])]
+        d[0] += float(r["TotalDurationNs"])
+        d[1] += int(r["Calls"])
+    g = lambda cs, k: cs[k][0] / cs[k][1] if cs.get(k) and cs[k][1] else float("nan")
+    print("| kernel class | avg us | waves waiting (any) | waiting on a dependency | on LDS | MFMA busy per SIMD | "
+          "LDS bank-conflict cycles / LDS instr | L2 reads / dispatch | avg L2 read latency (cycles) | "
+          "L2 reads in flight per CU | L1 pending-stall share |")
+    print("|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|")
+    for k, cs in sorted(acc.items(), key=lambda kv: -(dur[kv[0]][0] if dur[kv[0]][1] else 0)):
+        if not dur[k][1] or "SQ_WAVE_CYCLES" not in cs:
+            continue
+        us = dur[k][0] / dur[k][1] / 1e3
+        cyc = us * 1e-6 * 2.4e9
+        wave = g(cs, "SQ_WAVE_CYCLES")
+        req, lat = g(cs, "TCP_TCC_READ_REQ_sum"), g(cs, "TCP_TCC_READ_REQ_LATENCY_sum")
+        if not (wave > 0 and req > 0):
+            continue
+        print(f"| {k} | {us:.2f} | {g(cs, 'SQ_WAIT_ANY') / wave:.2f} | {g(cs, 'SQ_WAIT_INST_ANY') / wave:.2f} | "
+              f"{g(cs, 'SQ_WAIT_INST_LDS') / wave:.3f} | {g(cs, 'SQ_VALU_MFMA_BUSY_CYCLES') / (cyc * 1024):.3f} | "
+              f"{g(cs, 'SQ_LDS_BANK_CONFLICT') / max(g(cs, 'SQ_INSTS_LDS'), 1):.3f} | {req:.4g} | {lat / req:.0f} | "
+              f"{lat / (cyc * 256):.1f} | {g(cs, 'TCP_PENDING_STALL_CYCLES_sum') / (cyc * 256):.2f} |")
 
 
 # ----------------------------------------------------------------------------- algorithmic work
@@ -647,6 +694,9 @@ def main():
         return
     if args.summarize_mfma:
         summarize_mfma(*args.summarize_mfma)
+        return
+    if args.summarize_stalls:
+        summarize_stalls(*args.summarize_stalls)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (each MI355X would run its "
