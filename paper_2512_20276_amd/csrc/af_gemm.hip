@@ -637,9 +637,9 @@ __global__ __launch_bounds__(256, 1) void gemm32x2_kernel(GemmArgs a) {
   }
 }
 
-// NW-wave variant for 161..320 rows: the tile is 160 rows x 32 NW columns, each wave owning one
-// 32-column weight block over all five row blocks, so no weight fragment is loaded twice and
-// two row tiles fill the GPU where 288 x 128 tiles leave part of it idle.  Activations go
+// NW-wave variant for 161..384 rows: the tile is 32 FM rows (FM = 5 or 6) x 32 NW columns, each
+// wave owning one 32-column weight block over all FM row blocks, so no weight fragment is loaded
+// twice and two row tiles fill the GPU where 288 x 128 tiles leave part of it idle.  Activations go
 // through the LDS ring by DMA (issued by some of the waves, see below; every wave waits for its
 // own loads and then the barrier), the weights stream into per-wave register rings as in
 // gemm32x2_kernel.
@@ -783,48 +783,75 @@ __global__ __launch_bounds__(64 * NW, 1) void gemm32c_kernel(GemmArgs a) {
   }
 }
 
-// The 160-row tiles are taken at 161..320 rows in two cases:
+// The 160-row tiles (192-row tiles from 321 to 384 rows, so that two row tiles still hold every
+// row) are taken in two cases:
 //  * six waves (192 columns), unsplit or split two ways over K, when that fills 3/4 of the GPU
 //    or more in one pass (a 7B-shape step's gate/up projection: 2 x 115 = 230 workgroups; QKV:
 //    2 x 64 x 2 = 256);
 //  * four waves (128 columns) for narrow projections (N <= 4096) split four ways over K (the
 //    output and down projections: 2 x 32 x 4 = 256 workgroups), which write half the fp32
 //    partial sums of the 8-way split the 288 x 128 tile needs to fill the GPU.
-constexpr int C6_FM = 5, C6_NW = 6;
+constexpr int C6_NW = 6;
+// 32-row blocks per row tile: 5 for 6..10 blocks, 6 for 11..12, else none.
+static int c6_fm(int M) {
+  const int mb = (M + 31) / 32;
+  return mb > 5 && mb <= 10 ? 5 : mb > 10 && mb <= 12 ? 6 : 0;
+}
 static int c6_narrow(int M, int N, int Kp) {
-  const int mb = (M + 31) / 32, nb = (N + 31) / 32, units = Kp / 256;
-  if (mb <= C6_FM || mb > 2 * C6_FM || nb > 128 || units < 4) return 0;
+  const int fm = c6_fm(M), nb = (N + 31) / 32, units = Kp / 256;
+  if (!fm || nb > 128 || units < 4) return 0;
   const int S = 4, per = (units + S - 1) / S;
   return (units + per - 1) / per;
 }
-static bool use_c6(const GemmArgs& a) {
-  const int mb = (a.M + 31) / 32, nb = (a.N + 31) / 32;
-  const int wgs = ((mb + C6_FM - 1) / C6_FM) * ((nb + C6_NW - 1) / C6_NW) * a.splits;
+// Split-K factor of the six-wave plan: 1 or 2, whichever puts 192..256 workgroups in one pass
+// (0: the plan does not fit).
+static int c6_wide_splits(int M, int N, int Kp) {
+  const int fm = c6_fm(M);
+  if (!fm) return 0;
+  const int mb = (M + 31) / 32, nb = (N + 31) / 32;
+  const int tiles = ((mb + fm - 1) / fm) * ((nb + C6_NW - 1) / C6_NW);
+  if (tiles >= 192 && tiles <= 256) return 1;
+  if (2 * tiles >= 192 && 2 * tiles <= 256 && Kp / 256 >= 2) return 2;
+  return 0;
+}
+static bool use_c6(int epi, const GemmArgs& a) {
+  const int fm = c6_fm(a.M);
+  if (!fm || (fm == 6 && epi == EPI_STORE_F32 && a.splits == 1)) return false;
   if (a.splits > 1 && a.splits == c6_narrow(a.M, a.N, a.Kp)) return true;
-  return a.splits <= 2 && mb > C6_FM && mb <= 2 * C6_FM && wgs >= 192 && wgs <= 256;
+  return a.splits == c6_wide_splits(a.M, a.N, a.Kp);
 }
 
-static hipError_t gemm32c_launch(int epi, const GemmArgs& a, hipStream_t s) {
+template <int FM>
+static hipError_t gemm32c_launch_fm(int epi, const GemmArgs& a, hipStream_t s) {
   const int mb = (a.M + 31) / 32, nb = (a.N + 31) / 32;
-  if (a.splits > 1 && a.splits == c6_narrow(a.M, a.N, a.Kp)) {  // narrow: four-wave 160 x 128 tile
-    const dim3 grid(((mb + C6_FM - 1) / C6_FM) * ((nb + 3) / 4) * a.splits);
-    hipLaunchKernelGGL((gemm32c_kernel<C6_FM, 4, EPI_STORE>), grid, dim3(256), 0, s, a);
+  if (a.splits > 1 && a.splits == c6_narrow(a.M, a.N, a.Kp)) {  // narrow: four-wave FM x 4 block tile
+    const dim3 grid(((mb + FM - 1) / FM) * ((nb + 3) / 4) * a.splits);
+    hipLaunchKernelGGL((gemm32c_kernel<FM, 4, EPI_STORE>), grid, dim3(256), 0, s, a);
     return hipGetLastError();
   }
-  const dim3 grid(((mb + C6_FM - 1) / C6_FM) * ((nb + C6_NW - 1) / C6_NW) * a.splits), block(64 * C6_NW);
+  const dim3 grid(((mb + FM - 1) / FM) * ((nb + C6_NW - 1) / C6_NW) * a.splits), block(64 * C6_NW);
   if (a.splits > 1) {  // partial sums only: one instance serves every epilogue
-    hipLaunchKernelGGL((gemm32c_kernel<C6_FM, C6_NW, EPI_STORE>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((gemm32c_kernel<FM, C6_NW, EPI_STORE>), grid, block, 0, s, a);
     return hipGetLastError();
   }
   switch (epi) {
-    case EPI_STORE: hipLaunchKernelGGL((gemm32c_kernel<C6_FM, C6_NW, EPI_STORE>), grid, block, 0, s, a); break;
-    case EPI_STORE_F32: hipLaunchKernelGGL((gemm32c_kernel<C6_FM, C6_NW, EPI_STORE_F32>), grid, block, 0, s, a); break;
-    case EPI_RESID: hipLaunchKernelGGL((gemm32c_kernel<C6_FM, C6_NW, EPI_RESID>), grid, block, 0, s, a); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((gemm32c_kernel<C6_FM, C6_NW, EPI_SWIGLU>), grid, block, 0, s, a); break;
-    case EPI_QKV: hipLaunchKernelGGL((gemm32c_kernel<C6_FM, C6_NW, EPI_QKV>), grid, block, 0, s, a); break;
+    case EPI_STORE: hipLaunchKernelGGL((gemm32c_kernel<FM, C6_NW, EPI_STORE>), grid, block, 0, s, a); break;
+    case EPI_RESID: hipLaunchKernelGGL((gemm32c_kernel<FM, C6_NW, EPI_RESID>), grid, block, 0, s, a); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm32c_kernel<FM, C6_NW, EPI_SWIGLU>), grid, block, 0, s, a); break;
+    case EPI_QKV: hipLaunchKernelGGL((gemm32c_kernel<FM, C6_NW, EPI_QKV>), grid, block, 0, s, a); break;
+    case EPI_STORE_F32:
+      if constexpr (FM == 5) {
+        hipLaunchKernelGGL((gemm32c_kernel<FM, C6_NW, EPI_STORE_F32>), grid, block, 0, s, a);
+        break;
+      }
+      return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+static hipError_t gemm32c_launch(int epi, const GemmArgs& a, hipStream_t s) {
+  return c6_fm(a.M) == 6 ? gemm32c_launch_fm<6>(epi, a, s) : gemm32c_launch_fm<5>(epi, a, s);
 }
 
 // 32-row blocks per tile: the smallest tile that holds every row (up to 10 blocks, 320 rows;
@@ -869,7 +896,7 @@ static hipError_t gemm_dispatch_bf16(int epi, const GemmArgs& a, hipStream_t s) 
   if (a.astride <= 0 || a.Kp % 256 != 0 || a.astride < (long)a.Kp * 32 || a.bstride < (long)a.Kp * 32)
     return hipErrorInvalidValue;
   hipError_t e;
-  if (use_c6(a)) {
+  if (use_c6(epi, a)) {
     e = gemm32c_launch(epi, a, s);
     if (e != hipSuccess || a.splits <= 1 || a.partials_only) return e;
     return reduce_launch<bf16>(epi, a, s);
@@ -889,6 +916,7 @@ static hipError_t gemm_dispatch_bf16(int epi, const GemmArgs& a, hipStream_t s) 
 int gemm_splits(int dtype, int M, int N, int Kp) {
   if (dtype == AF_BF16) {
     if (const int S = c6_narrow(M, N, Kp)) return S;
+    if (const int S = c6_wide_splits(M, N, Kp)) return S;
     const int fm = fm_for(M);
     const int tiles = (((M + 31) / 32 + fm - 1) / fm) * (((N + 31) / 32 + 3) / 4);
     return splits_for(tiles, Kp / gemm_k_align());

@@ -71,10 +71,11 @@ def test_linear(storage, M, N, K):
                   rtol=8e-3 if storage == "bf16" else 1e-5)
 
 
-@pytest.mark.parametrize("M", [161, 200, 282, 291, 320])
+@pytest.mark.parametrize("M", [161, 200, 282, 291, 320, 326, 351, 384])
 def test_linear_qkv_width_split_k(M):
-    """N = 12288, K = 4096 (the QKV projection's width) at 161..320 rows: a two-way K split on the
-    six-wave 160 x 192 tile, two row tiles, ragged rows; partial sums and reduce against fp64."""
+    """N = 12288, K = 4096 (the QKV projection's width) at 161..384 rows: a two-way K split on the
+    six-wave 160 x 192 tile (192 x 192 from 321 rows), two row tiles, ragged rows; partial sums
+    and reduce against fp64."""
     N, K = 12288, 4096
     x = wl.draw(("t_lin_x", M, K), (M, K), device="cuda")
     w = wl.draw(("t_lin_w", N, K), (N, K), std=0.02, device="cuda")
@@ -85,12 +86,13 @@ def test_linear_qkv_width_split_k(M):
     _assert_close(y, ref, "bf16", "linear", min_exact=0.99, atol=1e-3, rtol=8e-3)
 
 
-@pytest.mark.parametrize("M", [161, 282, 320])
+@pytest.mark.parametrize("M", [161, 282, 320, 326, 384])
 @pytest.mark.parametrize("K", [4096, 11008])
 def test_linear_narrow_split_k(M, K):
-    """N = 4096 (the output and down projections' width) at 161..320 rows: the four-wave
-    160 x 128 tile split four ways over K (K = 11008: splits of 11 and 10 k units), two row
-    tiles with a ragged second one; partial sums and reduce against fp64."""
+    """N = 4096 (the output and down projections' width) at 161..384 rows: the four-wave
+    160 x 128 tile (192 x 128 from 321 rows) split four ways over K (K = 11008: splits of 11
+    and 10 k units), two row tiles with a ragged second one; partial sums and reduce against
+    fp64."""
     N = 4096
     x = wl.draw(("t_lin_x", M, K), (M, K), device="cuda")
     w = wl.draw(("t_lin_w", N, K), (N, K), std=0.02, device="cuda")
@@ -229,7 +231,7 @@ def test_qkv_rope_write_and_untouched_ring(shape_name):
 
 
 @pytest.mark.parametrize("shape_name", ["tiny", "7b"])
-@pytest.mark.parametrize("M", [1, 34, 282])
+@pytest.mark.parametrize("M", [1, 34, 282, 343])
 def test_mlp_and_residual_steps(shape_name, M):
     shape = (wl.TINY if shape_name == "tiny" else wl.LLAMA7B).with_layers(1)
     storage, dt, D, F = shape.dtype, shape.torch_dtype, shape.d_model, shape.d_ff
