@@ -200,34 +200,38 @@ def _logits_report(got, ref):
 
 
 @pytest.mark.timeout(1200)
-def test_7b_32_layer_pipeline_matches_oracle(monkeypatch):
-    """The benchmark workload (32 layers, K = 7, 8 slots) against the oracle pipeline.
+@pytest.mark.parametrize("K", [7, 16])
+def test_7b_32_layer_pipeline_matches_oracle(monkeypatch, K):
+    """The benchmark workload (32 layers, K = 7, 8 slots) and the K sweep's K = 16 point (17
+    slots) against the oracle pipeline.
 
-    The GPU pipeline runs steps 0..6 on its own greedy tokens; the oracle pipeline (Alg. 1 over
-    the float64 packed forward with bf16 storage) runs the same steps forced with the GPU's
-    tokens, so the two trajectories never part.  Step 6 is the first full step: a 276-row
-    prefill and six decode rows at contexts 277..282 (M = 282).
-      * Per layer (the gate): each of the 32 layers of step 6 runs on the GPU from the
+    The GPU pipeline runs steps 0..K-1 on its own greedy tokens; the oracle pipeline (Alg. 1
+    over the float64 packed forward with bf16 storage) runs the same steps forced with the
+    GPU's tokens, so the two trajectories never part.  Step K-1 is the first full step: a
+    276-row prefill and K-1 decode rows at contexts 277..276+K-1 (M = 282 at K = 7, 291 at
+    K = 16).
+      * Per layer (the gate): each of the 32 layers of step K-1 runs on the GPU from the
         oracle's input to that layer, with the oracle's ring history of that layer, and is held
         to the layer gate (max-abs 2e-2 / rel 1e-2 elementwise, normwise and per row).
       * Head: the final norm, LM head and argmax run on the oracle's last hidden rows of every
         step, and the last layer plus the head on the oracle's input to the last layer at step
-        6: logits elementwise to 2e-2 + 1e-2 |ref|; greedy tokens equal wherever the oracle's
+        K-1: logits elementwise to 2e-2 + 1e-2 |ref|; greedy tokens equal wherever the oracle's
         top-2 margin exceeds min(2 x the row's largest logit deviation, 0.05) (near-ties inside
-        that window are counted and bounded).
-      * Growth: the 32 layers of step 6 chained on the GPU's own outputs from the oracle's
+        that window are counted and bounded: at most 2, or a tenth of the tokens checked).
+      * Growth: the 32 layers of step K-1 chained on the GPU's own outputs from the oracle's
         layer-0 input (error growth per layer inside one step), reported.
       * End to end: every step's hidden rows and logits of the free-running pipeline.  Both
         sides store bf16 after every layer, and a summation order that differs (fp32 MFMA against
         float64) flips roundings that later layers mix into every element, so 32 layers drift.
         The drift allowed is set by a second implementation of the same definition: the oracle
         with its matrix products accumulated in float32 instead of float64, run over the same
-        32 layers of step 6.  The GPU's hidden rows and logits may drift from the float64 oracle
+        32 layers of step K-1.  The GPU's hidden rows and logits may drift from the float64 oracle
         at most twice as far (normwise) as that float32 oracle does; tokens must agree outside
         twice the observed logit deviation, and the capped-window count is reported.
     """
     shape = wl.LLAMA7B
-    K, L_V, L_T, n_slots, max_pos = 7, 256, 20, 8, 288
+    L_V, L_T = 256, 20
+    n_slots, max_pos = (8, 288) if K == 7 else (K + 1, L_V + L_T + K)
     L_P, H, hd, V = L_V + L_T, shape.n_heads, shape.head_dim, shape.vocab
     g, layers, w = _weights(shape)
     text = wl.draw_ids(("instruction", 0), L_T, shape.vocab, device="cuda")
@@ -249,7 +253,7 @@ def test_7b_32_layer_pipeline_matches_oracle(monkeypatch):
         gpu.append(dict(segments=res.segments, hidden=to_np(res.hidden), logits=to_np(res.logits),
                         tokens=res.tokens.cpu().tolist()))
     ring.close()
-    assert gpu[-1]["hidden"].shape[0] == 282
+    assert gpu[-1]["hidden"].shape[0] == L_P + K - 1
     emb = {t: to_np(prefill_embeds(t)[:L_P]) for t in range(K)}
     ids = pids.cpu().numpy().astype(np.int64)
     del pool
@@ -298,14 +302,14 @@ def test_7b_32_layer_pipeline_matches_oracle(monkeypatch):
           capped_flips, flush=True)
     assert len(trace) == shape.n_layers
 
-    # ---- per layer, from the oracle's input and ring history (step 6)
-    segs6 = gpu[K - 1]["segments"]
+    # ---- per layer, from the oracle's input and ring history (step K - 1)
+    segs_last = gpu[K - 1]["segments"]
     lring = af.Ring(shape.n_layers, n_slots, max_pos, H, hd, dtype=torch.bfloat16)
-    for sg in sorted(segs6, key=lambda s: s[4]):      # request r holds slot r, as in the pipeline
+    for sg in sorted(segs_last, key=lambda s: s[4]):      # request r holds slot r, as in the pipeline
         if sg[3] > 0:
             lring.append(sg[4], sg[3])
-    segs = reserve_step(lring, [(sg[4], sg[3], sg[1]) for sg in segs6])
-    assert [s[:4] for s in segs] == [s[:4] for s in segs6]
+    segs = reserve_step(lring, [(sg[4], sg[3], sg[1]) for sg in segs_last])
+    assert [s[:4] for s in segs] == [s[:4] for s in segs_last]
     per_layer, growth = [], []
     for l in range(shape.n_layers):
         for sg in segs:
@@ -320,8 +324,8 @@ def test_7b_32_layer_pipeline_matches_oracle(monkeypatch):
         per_layer.append(_layer_report(xl, trace[l]["x"], trace[l]))
         print("layer", l, "from the oracle's input", per_layer[-1], flush=True)
     # last layer + head from the oracle's input to the last layer
-    z, tok = gpu_head(xl, segs6)
-    ost_z = opipe.model.logits(trace[-1]["x"][[s[0] + s[1] - 1 for s in segs6]])
+    z, tok = gpu_head(xl, segs_last)
+    ost_z = opipe.model.logits(trace[-1]["x"][[s[0] + s[1] - 1 for s in segs_last]])
     last = _logits_report(z, ost_z)
     ties_last = check_tokens(tok, ost_z, z)
     print("last layer + head from the oracle's input", {k: last[k] for k in ("ok", "max_abs", "rms", "n_bad")},
@@ -341,14 +345,14 @@ def test_7b_32_layer_pipeline_matches_oracle(monkeypatch):
         return (np.asarray(x, np.float32) @ np.asarray(wt, np.float32).T).astype(np.float64)
 
     monkeypatch.setattr(om, "linear", linear_f32)
-    osegs = oracle_segments(segs6)
+    osegs = oracle_segments(segs_last)
     x = trace[0]["x_in"]
     floor = []
     for l in range(shape.n_layers):
         x = opipe.model.layer_packed(l, x, osegs, opipe.kv)
         floor.append(_layer_report(x, trace[l]["x"]))
         print("layer", l, "float32-accumulating oracle", floor[-1], flush=True)
-    z32 = opipe.model.logits(x[[s[0] + s[1] - 1 for s in segs6]])
+    z32 = opipe.model.logits(x[[s[0] + s[1] - 1 for s in segs_last]])
     monkeypatch.undo()
     floor_z = _logits_report(z32, ost_z)
     print("float32-accumulating oracle logits", {k: floor_z[k] for k in ("max_abs", "rms", "norm_rel", "n_bad")},
@@ -358,7 +362,7 @@ def test_7b_32_layer_pipeline_matches_oracle(monkeypatch):
     assert not bad, bad
     assert last["ok"], last
     assert all(h["ok"] for h in head), head
-    assert ties_head + ties_last <= 2, (ties_head, ties_last)
+    assert ties_head + ties_last <= max(2, (n_head + len(segs_last)) // 10), (ties_head, ties_last, n_head)
     h_floor, z_floor = floor[-1]["norm_rel"], floor_z["norm_rel"]
     for r in e2e:
         assert r["hidden"]["norm_rel"] <= 2 * h_floor and r["logits"]["norm_rel"] <= 2 * z_floor, (r, h_floor, z_floor)
