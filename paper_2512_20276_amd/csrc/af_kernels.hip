@@ -13,7 +13,8 @@ namespace af {
 constexpr int NORM_THREADS = 512;
 
 // Sum over the workgroup of one value per thread, in a fixed order (lanes by xor shuffles, then
-// the waves in order); the same order in every kernel that normalises a row.
+// the waves in order); the same order in every kernel that normalises a row, whose squares are
+// accumulated with explicit fused multiply-adds so that every such kernel rounds alike.
 __device__ __forceinline__ float norm_block_sum(float v, float* red) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
@@ -41,12 +42,12 @@ __global__ __launch_bounds__(NORM_THREADS) void rmsnorm_kernel(const T* __restri
       T v[V];
       *(uint4*)v = *(const uint4*)(xr + i);
 #pragma unroll
-      for (int e = 0; e < V; ++e) ss += to_f(v[e]) * to_f(v[e]);
+      for (int e = 0; e < V; ++e) ss = fmaf(to_f(v[e]), to_f(v[e]), ss);
     }
   } else {
     for (int i = threadIdx.x; i < D; i += NORM_THREADS) {
       const float v = to_f(xr[i]);
-      ss += v * v;
+      ss = fmaf(v, v, ss);
     }
   }
   const float tot = norm_block_sum(ss, red);
@@ -125,7 +126,7 @@ __global__ __launch_bounds__(NORM_THREADS) void resid_norm_kernel(const float* _
       for (int e = 0; e < 8; ++e) r[e] = from_f<T>(to_f(res[e]) + v[e]);
       store8<T>(xr + i, r);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) ss += to_f(r[e]) * to_f(r[e]);
+      for (int e = 0; e < 8; ++e) ss = fmaf(to_f(r[e]), to_f(r[e]), ss);
     }
   } else {
     for (int i = threadIdx.x; i < D; i += NORM_THREADS) {
@@ -133,7 +134,7 @@ __global__ __launch_bounds__(NORM_THREADS) void resid_norm_kernel(const float* _
       for (int sp = 0; sp < splits; ++sp) v += partial[sp * plane + (size_t)m * D + i];
       const T r = from_f<T>(to_f(xr[i]) + v);
       xr[i] = r;
-      ss += to_f(r) * to_f(r);
+      ss = fmaf(to_f(r), to_f(r), ss);
     }
   }
   const float tot = norm_block_sum(ss, red);
