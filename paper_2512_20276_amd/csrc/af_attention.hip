@@ -239,16 +239,18 @@ __device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int ti
   constexpr int KPT = NCH;               // values: keys per thread
   constexpr int KGV = ATTN_BKV / KPT;    // values: key groups
   static_assert(KGV * CPR == 256, "value mapping");
+  // Keys past kv_end are loaded from the last visible key (unconditional loads, so nothing waits
+  // for them until the tile is parked) and replaced by zeros when the tile is parked.
   uint4 kreg[NCH], vreg[NCH];
   const int kc = tid % CPR, kr = tid / CPR;
   const int vg = tid % KGV, vc = tid / KGV;
   auto load_tile = [&](int kb0) {
 #pragma unroll
     for (int j = 0; j < NCH; ++j) {
-      const int key = kb0 + kr + KR * j;
-      kreg[j] = key < kv_end ? *(const uint4*)(Kg + (size_t)key * HD + kc * VEC) : zero4();
-      const int vkey = kb0 + vg * KPT + j;
-      vreg[j] = vkey < kv_end ? *(const uint4*)(Vg + (size_t)vkey * HD + vc * VEC) : zero4();
+      const int key = min(kb0 + kr + KR * j, kv_end - 1);
+      kreg[j] = *(const uint4*)(Kg + (size_t)key * HD + kc * VEC);
+      const int vkey = min(kb0 + vg * KPT + j, kv_end - 1);
+      vreg[j] = *(const uint4*)(Vg + (size_t)vkey * HD + vc * VEC);
     }
   };
   const int n_kt = (kv_end + ATTN_BKV - 1) / ATTN_BKV;
@@ -261,18 +263,22 @@ __device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int ti
     for (int d = 0; d < DB; ++d) oacc[d] = f32x4{0.f, 0.f, 0.f, 0.f};
     m_run = -INFINITY;
     l_run = 0.f;
-    load_tile(grp * ATTN_BKV);        // keys past kv_end load as zeros
+    load_tile(grp * ATTN_BKV);
     for (int it = 0; it < n_it; ++it) {
       const int kt = 2 * it + grp;
       const int kb0 = kt * ATTN_BKV;
       // ---- park the tile in LDS: keys row-major, values transposed
       __syncthreads();  // the previous tile's LDS reads are done
 #pragma unroll
-      for (int j = 0; j < NCH; ++j) *(uint4*)(&Ks[(kr + KR * j) * KROW + kc * VEC]) = kreg[j];
+      for (int j = 0; j < NCH; ++j)
+        *(uint4*)(&Ks[(kr + KR * j) * KROW + kc * VEC]) = kb0 + kr + KR * j < kv_end ? kreg[j] : zero4();
       {
         T vt[NCH][VEC];
 #pragma unroll
-        for (int j = 0; j < NCH; ++j) __builtin_memcpy(vt[j], &vreg[j], 16);
+        for (int j = 0; j < NCH; ++j) {
+          const uint4 v = kb0 + vg * KPT + j < kv_end ? vreg[j] : zero4();
+          __builtin_memcpy(vt[j], &v, 16);
+        }
 #pragma unroll
         for (int e = 0; e < VEC; ++e) {
           T col[KPT];
