@@ -89,9 +89,31 @@ __device__ __forceinline__ void epi_group8(const GemmArgs& a, int m, int nc, con
   }
 }
 
+// What the QKV epilogue needs besides the sums for one 16-column group of row m: the region
+// (queries, keys, values), head, rotary offset, the row's ring slot and position, and the
+// rotary (cos, sin) pairs; loaded ahead of the sums where the sums come from memory.
+struct QkvRow {
+  int region, h, dj, slot, pos;
+  float cs[16];
+  __device__ __forceinline__ void load(const GemmArgs& a, int m, int c) {
+    const int D = a.d_model, hd = a.head_dim, half = hd >> 1;
+    region = c / D;
+    const int cr = c - region * D;
+    h = cr / hd;
+    dj = ((cr - h * hd) >> 4) * 8;
+    slot = a.row_sp[2 * m];
+    pos = a.row_sp[2 * m + 1];
+    if (region != 2) {
+      load8<float>(a.rope_cs + ((size_t)pos * half + dj) * 2, cs);
+      load8<float>(a.rope_cs + ((size_t)pos * half + dj) * 2 + 8, cs + 8);
+    }
+  }
+};
+
 // The 16-column group starting at c (c % 16 == 0): a-columns c .. c+7, partners c+8 .. c+15.
 template <typename T, int EPI>
-__device__ __forceinline__ void epi_group16(const GemmArgs& a, int m, int c, const float* va, const float* vb) {
+__device__ __forceinline__ void epi_group16(const GemmArgs& a, int m, int c, const float* va, const float* vb,
+                                            const QkvRow* pre = nullptr) {
   T r0[8], r1[8];
   if constexpr (EPI == EPI_SWIGLU) {
     const int f = (c >> 4) * 8;
@@ -99,32 +121,29 @@ __device__ __forceinline__ void epi_group16(const GemmArgs& a, int m, int c, con
     for (int e = 0; e < 8; ++e) r0[e] = from_f<T>(va[e] / (1.0f + __expf(-va[e])) * vb[e]);
     store8<T>((T*)a.out + (a.ostride > 0 ? frag_off(m, f, a.ostride) : (size_t)m * a.ldo + f), r0);
   } else {  // EPI_QKV: rotary pairs (dj + e, dj + e + hd/2), e < 8
-    const int D = a.d_model, hd = a.head_dim, half = hd >> 1;
-    const int region = c / D, cr = c - region * D;
-    const int h = cr / hd, dj = ((cr - h * hd) >> 4) * 8;
-    const int slot = a.row_sp[2 * m], pos = a.row_sp[2 * m + 1];
+    QkvRow q;
+    if (pre) q = *pre;
+    else q.load(a, m, c);
+    const int hd = a.head_dim, half = hd >> 1;
     T* dst;
-    if (region == 2) {
-      dst = (T*)a.ring_v + (((size_t)slot * a.n_heads + h) * a.max_pos + pos) * hd;
+    if (q.region == 2) {
+      dst = (T*)a.ring_v + (((size_t)q.slot * a.n_heads + q.h) * a.max_pos + q.pos) * hd;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         r0[e] = from_f<T>(va[e]);
         r1[e] = from_f<T>(vb[e]);
       }
     } else {
-      float cs[16];
-      load8<float>(a.rope_cs + ((size_t)pos * half + dj) * 2, cs);
-      load8<float>(a.rope_cs + ((size_t)pos * half + dj) * 2 + 8, cs + 8);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        r0[e] = from_f<T>(va[e] * cs[2 * e] - vb[e] * cs[2 * e + 1]);
-        r1[e] = from_f<T>(vb[e] * cs[2 * e] + va[e] * cs[2 * e + 1]);
+        r0[e] = from_f<T>(va[e] * q.cs[2 * e] - vb[e] * q.cs[2 * e + 1]);
+        r1[e] = from_f<T>(vb[e] * q.cs[2 * e] + va[e] * q.cs[2 * e + 1]);
       }
-      dst = region == 0 ? (T*)a.out + (size_t)m * a.ldo + h * hd
-                        : (T*)a.ring_k + (((size_t)slot * a.n_heads + h) * a.max_pos + pos) * hd;
+      dst = q.region == 0 ? (T*)a.out + (size_t)m * a.ldo + q.h * hd
+                          : (T*)a.ring_k + (((size_t)q.slot * a.n_heads + q.h) * a.max_pos + q.pos) * hd;
     }
-    store8<T>(dst + dj, r0);
-    store8<T>(dst + dj + half, r1);
+    store8<T>(dst + q.dj, r0);
+    store8<T>(dst + q.dj + half, r1);
   }
 }
 
@@ -262,19 +281,37 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs a) {
   if (idx >= (size_t)a.M * per_row) return;
   const int m = (int)(idx / per_row), c = (int)(idx % per_row) * W;
   const size_t plane = (size_t)a.M * a.N;
+  // every load is issued before any sum waits on one: the epilogue's row data, then all the
+  // partial sums (up to MAXS splits at once); they are added in split order
+  QkvRow q;
+  if constexpr (EPI == EPI_QKV) q.load(a, m, c);
+  constexpr int MAXS = 4;
+  float t[MAXS][W];
+#pragma unroll
+  for (int sp = 0; sp < MAXS; ++sp)
+    if (sp < a.splits) {
+      const float* src = a.partial + sp * plane + (size_t)m * a.N + c;
+      load8<float>(src, t[sp]);
+      if constexpr (paired) load8<float>(src + 8, t[sp] + 8);
+    }
   float v[W];
 #pragma unroll
   for (int e = 0; e < W; ++e) v[e] = 0.f;
-  for (int sp = 0; sp < a.splits; ++sp) {
-    float t[W];
-    const float* src = a.partial + sp * plane + (size_t)m * a.N + c;
-    load8<float>(src, t);
-    if constexpr (paired) load8<float>(src + 8, t + 8);
 #pragma unroll
-    for (int e = 0; e < W; ++e) v[e] += t[e];
+  for (int sp = 0; sp < MAXS; ++sp)
+    if (sp < a.splits)
+#pragma unroll
+      for (int e = 0; e < W; ++e) v[e] += t[sp][e];
+  for (int sp = MAXS; sp < a.splits; ++sp) {
+    float u[W];
+    const float* src = a.partial + sp * plane + (size_t)m * a.N + c;
+    load8<float>(src, u);
+    if constexpr (paired) load8<float>(src + 8, u + 8);
+#pragma unroll
+    for (int e = 0; e < W; ++e) v[e] += u[e];
   }
   if constexpr (paired)
-    epi_group16<T, EPI>(a, m, c, v, v + 8);
+    epi_group16<T, EPI>(a, m, c, v, v + 8, EPI == EPI_QKV ? &q : nullptr);
   else
     epi_group8<T, EPI>(a, m, c, v);
 }

@@ -97,6 +97,55 @@ __global__ __launch_bounds__(NORM_THREADS) void resid_norm_kernel(const float* _
   constexpr int V = 16 / sizeof(T);
   const bool vec = sizeof(T) == 2 && D % 8 == 0 && ldx % 8 == 0;
   float ss = 0.f;
+  if (vec && D <= NORM_THREADS * V) {
+    // at most one chunk per thread: every load (the partial sums of all splits, the residual
+    // row, the gain) is issued before anything waits, and the updated residual stays in
+    // registers for the normalisation; the same arithmetic, in the same order, as below
+    const int i = threadIdx.x * V;
+    const bool has = i < D;
+    constexpr int MAXS = 8;
+    float t[MAXS][8];
+    T res[8], gv[8];
+    if (has) {
+#pragma unroll
+      for (int sp = 0; sp < MAXS; ++sp)
+        if (sp < splits) load8<float>(partial + sp * plane + (size_t)m * D + i, t[sp]);
+      load8<T>(xr + i, res);
+      load8<T>(g + i, gv);
+    }
+    T r[8];
+    if (has) {
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = 0.f;
+#pragma unroll
+      for (int sp = 0; sp < MAXS; ++sp)
+        if (sp < splits)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] += t[sp][e];
+      for (int sp = MAXS; sp < splits; ++sp) {
+        float u[8];
+        load8<float>(partial + sp * plane + (size_t)m * D + i, u);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] += u[e];
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) r[e] = from_f<T>(to_f(res[e]) + v[e]);
+      store8<T>(xr + i, r);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss = fmaf(to_f(r[e]), to_f(r[e]), ss);
+    }
+    const float tot = norm_block_sum(ss, red);
+    const float inv = 1.0f / sqrtf(tot / (float)D + eps);
+    if (has) {
+      T o[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = from_f<T>(to_f(r[e]) * inv * to_f(gv[e]));
+      T* dst = ystride > 0 ? y + frag_off(m, i, ystride) : y + (size_t)m * ldy + i;
+      *(uint4*)dst = *(const uint4*)o;
+    }
+    return;
+  }
   if (vec) {
     for (int i = threadIdx.x * V; i < D; i += NORM_THREADS * V) {
       // all of this chunk's partial sums are requested before any is added (one memory latency
