@@ -115,6 +115,20 @@ def test_linear_large_m():
     _assert_close(y, ref, "bf16", "linear", min_exact=0.99, atol=1e-3, rtol=8e-3)
 
 
+@pytest.mark.parametrize("M,N", [(400, 22016), (2264, 4672)])
+def test_linear_wide_tile(M, N):
+    """Shapes that take the 288 x 256 tile (two row tiles of gate/up width; eight row tiles with
+    a last column tile half past N), against fp64."""
+    K = 4096
+    x = wl.draw(("t_lin_x", M, K), (M, K), device="cuda")
+    w = wl.draw(("t_lin_w", N, K), (N, K), std=0.02, device="cuda")
+    y = torch.full((M, N), float("nan"), dtype=torch.bfloat16, device="cuda")
+    af.op_linear(x, w, y)
+    torch.cuda.synchronize()
+    ref = round_storage(linear(to_np(x), to_np(w)), "bf16")
+    _assert_close(y, ref, "bf16", "linear", min_exact=0.99, atol=1e-3, rtol=8e-3)
+
+
 # ----------------------------------------------------------------------------- attention
 def _fill_ring(ring, layer, n_slots, max_pos, H, hd, dt, key):
     """N(0,1) K/V in every position of every slot; returns oracle-side copies [slot, pos, H, hd]."""
