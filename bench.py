@@ -96,9 +96,10 @@ def measured_traffic():
 def _kernel_class(name: str) -> str:
     """Maps a kernel name (mangled or demangled) to the label used in the summaries."""
     import re
-    if any(k in name for k in ("gemm_kernel", "gemm32_kernel", "gemm32x2_kernel", "gemm32c_kernel")):
-        epi = (re.search(r"gemm32(?:x2|c)?_kernelI(?:Li\d+E)*Li(\d+)EEEv", name)    # bf16, mangled
-               or re.search(r"gemm32(?:x2|c)?_kernel<[^>]*?(\d+)>", name)            # bf16, demangled
+    if any(k in name for k in ("gemm_kernel", "gemm32_kernel", "gemm32x2_kernel", "gemm32c_kernel",
+                               "gemm32w_kernel")):
+        epi = (re.search(r"gemm32(?:x2|c|w)?_kernelI(?:Li\d+E)*Li(\d+)EEEv", name)    # bf16, mangled
+               or re.search(r"gemm32(?:x2|c|w)?_kernel<[^>]*?(\d+)>", name)            # bf16, demangled
                or re.search(r",\s*(\d)>\s*\(", name) or re.search(r",\s*\(af::Epi\)(\d)>", name)
                or re.search(r"GemmCfgI(?:Li\d+E)+EELi(\d)E", name))                  # fp32 kernel
         e = int(epi.group(1)) if epi else -1

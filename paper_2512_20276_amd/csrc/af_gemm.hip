@@ -674,27 +674,27 @@ __global__ __launch_bounds__(256, 1) void gemm32x2_kernel(GemmArgs a) {
   }
 }
 
-// Wide tile for many rows: 32 FM rows x 256 columns on 4 RG waves, RG row groups x 4 column
-// groups of 64 (two 32-column weight blocks per wave, as in gemm32x2_kernel).  Per byte loaded
-// into the CU it does 1.5x the MFMA work of the 288 x 128 tile (288 + 256 bytes per row of K for
-// 288 x 256 outputs, against 288 + 128 for 288 x 128), which decides the time where the
-// concurrent L2 reads per CU bound the GEMM.  With FM = 9 and three row groups of three blocks
-// (twelve waves, three per SIMD) the accumulators take 96 registers of the 168 a wave has.
-// Activations by DMA (spread over all waves), weights two k steps ahead in registers, each k
-// step waiting for its own; the fp32 tile goes through the LDS ring one row group per pass.
-template <int FM, int RG, int EPI>
-__global__ __launch_bounds__(256 * RG, 1) void gemm32w_kernel(GemmArgs a) {
-  // weights: a ring of two k steps per wave, each step's weights loaded two steps ahead
-  constexpr int KS = 4, NBUF = 4, PFB = 2, BLK = 512, CG = 4, TN = 64 * CG, NWV = RG * CG;
-  constexpr int SB = FM * KS;  // fragment blocks per stage
-  static_assert(FM % RG == 0 && SB % NWV == 0 && KS % PFB == 0, "pipeline shape");
-  constexpr int MB = FM / RG;     // row blocks per row group
-  constexpr int D = SB / NWV;     // DMAs per stage per wave
+// Wide tile for many rows: 32 FM rows x 256 columns on eight waves, each owning one 32-column
+// weight block over all FM row blocks (as gemm32c_kernel does for 160 rows), so no weight
+// fragment is loaded twice.  Per byte loaded into the CU it does 1.5x the MFMA work of the
+// 288 x 128 tile (288 + 256 bytes per row of K for 288 x 256 outputs, against 288 + 128 for
+// 288 x 128).  The accumulators take 16 FM registers; one k step's activation fragments are
+// read at a time (the other wave on the SIMD covers the LDS latency), the weights run two k
+// steps ahead.  Activations by DMA from waves 0..3; the fp32 tile goes through the LDS ring
+// three row blocks per pass.  (Three row groups of four column groups, each wave two weight
+// blocks, measured no faster: each weight fragment was then requested once per row group.)
+template <int FM, int EPI>
+__global__ __launch_bounds__(512, 1) void gemm32w_kernel(GemmArgs a) {
+  constexpr int KS = 4, NBUF = 4, PFB = 2, BLK = 512, NW = 8, TN = 32 * NW, PB = 3;
+  constexpr int SB = FM * KS;        // fragment blocks per stage
+  constexpr int DW = SB / 4;         // DMAs per stage of each of waves 0..3
+  constexpr int NPASS = (FM + PB - 1) / PB;
+  static_assert(SB % 4 == 0 && KS % PFB == 0, "pipeline shape");
   __shared__ __attribute__((aligned(1024))) bf16 As[NBUF][SB * BLK];
-  static_assert(32 * MB * TN * 4 <= (int)sizeof(As), "a row group's fp32 tile must fit the stage buffers");
+  static_assert(32 * PB * TN * 4 <= (int)sizeof(As), "an epilogue pass must fit the stage buffers");
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, rg = wave / CG, cg = wave % CG;
-  const int n_blocks = (a.N + 31) >> 5, n_nt = (n_blocks + 2 * CG - 1) / (2 * CG);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n_blocks = (a.N + 31) >> 5, n_nt = (n_blocks + NW - 1) / NW;
   const int m_blocks = (a.M + 31) >> 5, n_mt = (m_blocks + FM - 1) / FM;
   const int S = a.splits;
   const int t = xcd_remap(blockIdx.x, n_mt * n_nt * S);
@@ -704,123 +704,116 @@ __global__ __launch_bounds__(256 * RG, 1) void gemm32w_kernel(GemmArgs a) {
   const int units = ks16 / (KS * NBUF), per = (units + S - 1) / S;
   const int kb = min(units, sp * per) * (KS * NBUF), ke = min(units, sp * per + per) * (KS * NBUF);
   const int n_st = (ke - kb) / KS;  // a multiple of NBUF
-  const bf16* bp0 = (const bf16*)a.B + (size_t)min(nt * 2 * CG + cg * 2, n_blocks - 1) * a.bstride + lane * 8;
-  const bf16* bp1 = (const bf16*)a.B + (size_t)min(nt * 2 * CG + cg * 2 + 1, n_blocks - 1) * a.bstride + lane * 8;
+  // this wave's weight block (past N: a valid block whose columns are never stored)
+  const bf16* bp = (const bf16*)a.B + (size_t)min(nt * NW + wave, n_blocks - 1) * a.bstride + lane * 8;
   const bf16* __restrict__ Ab = (const bf16*)a.A;
   float* T_ = (float*)&As[0][0];
   const int m0 = mt * FM * 32, n0 = nt * TN;
-  const int moff = rg * MB;  // this wave's first row block in the tile
 
-  auto dma = [&](auto buf, int st) {
-    static_for<0, D>([&](auto d) {
-      const int q = wave + NWV * decltype(d)::value, mb = q / KS, j = q % KS;
+  auto body = [&](auto d_c) {
+    constexpr int D = decltype(d_c)::value;  // DMAs per stage issued by this wave
+    auto dma = [&](auto buf, int st) {
+      static_for<0, D>([&](auto d) {
+        const int q = wave + 4 * decltype(d)::value, mb = q / KS, j = q % KS;
+        const int k = min(kb + st * KS + j, ks16 - 1);
+        const int blk = min(mt * FM + mb, m_blocks - 1);  // rows past M: a valid block, never stored
+        const bf16* src = Ab + (size_t)blk * a.astride + (size_t)k * BLK + lane * 8;
+        __builtin_amdgcn_global_load_lds((const void*)src,
+                                         (__attribute__((address_space(3))) void*)&As[buf][q * BLK], 16, 0, 0);
+      });
+    };
+    bf16x8 rb[PFB];
+    auto load_b = [&](auto slot, int st, int j) {
       const int k = min(kb + st * KS + j, ks16 - 1);
-      const int blk = min(mt * FM + mb, m_blocks - 1);  // rows past M: a valid block, never stored
-      const bf16* src = Ab + (size_t)blk * a.astride + (size_t)k * BLK + lane * 8;
-      __builtin_amdgcn_global_load_lds((const void*)src, (__attribute__((address_space(3))) void*)&As[buf][q * BLK],
-                                       16, 0, 0);
-    });
-  };
-  bf16x8 rb[PFB][2];
-  auto load_b = [&](auto slot, int st, int j) {
-    const int k = min(kb + st * KS + j, ks16 - 1);
-    const bf16* s0 = bp0 + (size_t)k * BLK;
-    const bf16* s1 = bp1 + (size_t)k * BLK;
-    bf16x8 v0, v1;
-    asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v0) : "v"(s0) : "memory");
-    asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v1) : "v"(s1) : "memory");
-    rb[slot][0] = v0;
-    rb[slot][1] = v1;
-  };
-  f32x16 acc[MB][2];
-  static_for<0, MB>([&](auto i) {
-    acc[i][0] = f32x16{};
-    acc[i][1] = f32x16{};
-  });
-  static_for<0, NBUF - 1>([&](auto b) {
-    dma(b, b);
-    __builtin_amdgcn_sched_barrier(0);
-  });
-  static_for<0, PFB>([&](auto j) { load_b(std::integral_constant<int, decltype(j)::value>{}, 0, j); });
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the loop's waits count from a full ring
-  __builtin_amdgcn_sched_barrier(0);
-
-  for (int st0 = 0; st0 < n_st; st0 += NBUF) {
-    static_for<0, NBUF>([&](auto u) {
-      constexpr int U = decltype(u)::value;
-      const int st = st0 + U;
-      // Loads complete in order.  Stage st's activations come from the DMA at the top of stage
-      // st - NBUF + 1, after which NBUF - 1 stages of weight loads (2 KS each) and NBUF - 2 DMAs
-      // were issued.  k step j's weights were loaded PFB steps earlier; after them came the
-      // 2 (PFB - 1) weight loads of the steps between and, when a stage top lies between, its DMAs.
-      constexpr int WAIT_A = 2 * KS * (NBUF - 1) + D * (NBUF - 2);
-      static_assert(WAIT_A <= 63, "vmcnt range");
-      asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(WAIT_A) : "memory");
-      dma(std::integral_constant<int, (U + NBUF - 1) % NBUF>{}, st + NBUF - 1);
+      const bf16* src = bp + (size_t)k * BLK;
+      bf16x8 v;
+      asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(src) : "memory");
+      rb[slot] = v;
+    };
+    f32x16 acc[FM];
+    static_for<0, FM>([&](auto i) { acc[i] = f32x16{}; });
+    static_for<0, NBUF - 1>([&](auto b) {
+      dma(b, b);
       __builtin_amdgcn_sched_barrier(0);
-      static_for<0, KS>([&](auto j) {
-        constexpr int J = decltype(j)::value;
-        constexpr int slot = (U * KS + J) % PFB;
-        bf16x8 af[MB];
-        static_for<0, MB>([&](auto i) {
-          af[i] = *(const bf16x8*)(&As[U][((moff + (int)decltype(i)::value) * KS + J) * BLK + lane * 8]);
-        });
-        constexpr int WAIT_B = 2 * (PFB - 1) + (J < PFB ? D : 0);
-        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(WAIT_B) : "memory");
-        __builtin_amdgcn_sched_barrier(0);
-        static_for<0, MB>([&](auto i) {
-          acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], rb[slot][0], acc[i][0], 0, 0, 0);
-          acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], rb[slot][1], acc[i][1], 0, 0, 0);
-        });
-        load_b(std::integral_constant<int, slot>{}, st + (J + PFB) / KS, (J + PFB) % KS);
-        __builtin_amdgcn_sched_barrier(0);
-      });
     });
-  }
-  // The ring's last (unused) loads land before any of its registers can be reused.
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-#pragma unroll
-  for (int p = 0; p < PFB; ++p) {
-    asm volatile("" : "+v"(rb[p][0]));
-    asm volatile("" : "+v"(rb[p][1]));
-  }
-
-  // ---- epilogue, one row group per pass through the stage buffers
-  constexpr bool paired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
-  constexpr int W = paired ? 16 : 8;
-  constexpr int ITEMS = 32 * MB * (TN / W);
-  for (int ps = 0; ps < RG; ++ps) {
-    __syncthreads();  // every wave's DMAs have landed and the buffers' last readers are done
-    if (rg == ps) {
-      static_for<0, MB>([&](auto i) {
-        static_for<0, 2>([&](auto n) {
-          static_for<0, 16>([&](auto r) {
-            constexpr int R = decltype(r)::value;
-            const int row = (int)decltype(i)::value * 32 + 8 * (R / 4) + 4 * (lane >> 5) + (R % 4);
-            T_[row * TN + cg * 64 + (int)decltype(n)::value * 32 + (lane & 31)] = acc[i][n][R];
+    static_for<0, PFB>([&](auto j) { load_b(std::integral_constant<int, decltype(j)::value>{}, 0, j); });
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the loop's waits count from a full ring
+    __builtin_amdgcn_sched_barrier(0);
+    for (int st0 = 0; st0 < n_st; st0 += NBUF) {
+      static_for<0, NBUF>([&](auto u) {
+        constexpr int U = decltype(u)::value;
+        const int st = st0 + U;
+        // Loads complete in order.  Stage st's activations come from the DMA at the top of stage
+        // st - NBUF + 1, after which NBUF - 1 stages of weight loads (KS each) and NBUF - 2 DMAs
+        // were issued.  k step j's weights were loaded PFB steps earlier; after them came the
+        // PFB - 1 weight loads of the steps between and, when a stage top lies between, its DMAs.
+        constexpr int WAIT_A = KS * (NBUF - 1) + D * (NBUF - 2);
+        static_assert(WAIT_A <= 63, "vmcnt range");
+        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(WAIT_A) : "memory");
+        dma(std::integral_constant<int, (U + NBUF - 1) % NBUF>{}, st + NBUF - 1);
+        __builtin_amdgcn_sched_barrier(0);
+        static_for<0, KS>([&](auto j) {
+          constexpr int J = decltype(j)::value;
+          constexpr int slot = (U * KS + J) % PFB;
+          bf16x8 af[FM];
+          static_for<0, FM>([&](auto i) {
+            af[i] = *(const bf16x8*)(&As[U][((int)decltype(i)::value * KS + J) * BLK + lane * 8]);
           });
+          constexpr int WAIT_B = (PFB - 1) + (J < PFB ? D : 0);
+          asm volatile("s_waitcnt vmcnt(%0)" ::"n"(WAIT_B) : "memory");
+          __builtin_amdgcn_sched_barrier(0);
+          static_for<0, FM>([&](auto i) {
+            acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], rb[slot], acc[i], 0, 0, 0);
+          });
+          load_b(std::integral_constant<int, slot>{}, st + (J + PFB) / KS, (J + PFB) % KS);
+          __builtin_amdgcn_sched_barrier(0);
         });
       });
     }
-    __syncthreads();
-    for (int it = tid; it < ITEMS; it += 64 * NWV) {
-      const int row = it / (TN / W), col = (it % (TN / W)) * W;
-      const int m = m0 + ps * MB * 32 + row, nc = n0 + col;
-      if (m >= a.M || nc >= a.N) continue;  // N % 16 == 0: a group is wholly inside or outside
-      float v[W];
+    // the ring's last (unused) loads land before any of its registers can be reused
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 #pragma unroll
-      for (int e = 0; e < W; e += 4) *(f32x4*)&v[e] = *(const f32x4*)&T_[row * TN + col + e];
-      if (S > 1) {
-        float* dst = a.partial + ((size_t)sp * a.M + m) * a.N + nc;
+    for (int p = 0; p < PFB; ++p) asm volatile("" : "+v"(rb[p]));
+
+    // ---- epilogue, PB row blocks per pass through the stage buffers
+    constexpr bool paired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
+    constexpr int W = paired ? 16 : 8;
+    static_for<0, NPASS>([&](auto p_c) {
+      constexpr int PS = decltype(p_c)::value;
+      constexpr int NB = PS * PB + PB <= FM ? PB : FM - PS * PB;  // row blocks in this pass
+      __syncthreads();  // every wave's DMAs have landed and the buffers' last readers are done
+      static_for<0, NB>([&](auto i) {
+        static_for<0, 16>([&](auto r) {
+          constexpr int R = decltype(r)::value;
+          const int row = (int)decltype(i)::value * 32 + 8 * (R / 4) + 4 * (lane >> 5) + (R % 4);
+          T_[row * TN + wave * 32 + (lane & 31)] = acc[PS * PB + decltype(i)::value][R];
+        });
+      });
+      __syncthreads();
+      constexpr int ITEMS = 32 * NB * (TN / W);
+      for (int it = tid; it < ITEMS; it += 64 * NW) {
+        const int row = it / (TN / W), col = (it % (TN / W)) * W;
+        const int m = m0 + PS * PB * 32 + row, nc = n0 + col;
+        if (m >= a.M || nc >= a.N) continue;  // N % 16 == 0: a group is wholly inside or outside
+        float v[W];
 #pragma unroll
-        for (int e = 0; e < W; e += 4) *(f32x4*)(dst + e) = *(const f32x4*)&v[e];
-      } else if constexpr (paired) {
-        epi_group16<bf16, EPI>(a, m, nc, v, v + 8);
-      } else {
-        epi_group8<bf16, EPI>(a, m, nc, v);
+        for (int e = 0; e < W; e += 4) *(f32x4*)&v[e] = *(const f32x4*)&T_[row * TN + col + e];
+        if (S > 1) {
+          float* dst = a.partial + ((size_t)sp * a.M + m) * a.N + nc;
+#pragma unroll
+          for (int e = 0; e < W; e += 4) *(f32x4*)(dst + e) = *(const f32x4*)&v[e];
+        } else if constexpr (paired) {
+          epi_group16<bf16, EPI>(a, m, nc, v, v + 8);
+        } else {
+          epi_group8<bf16, EPI>(a, m, nc, v);
+        }
       }
-    }
-  }
+    });
+  };
+  if (wave < 4)
+    body(std::integral_constant<int, DW>{});
+  else
+    body(std::integral_constant<int, 0>{});
 }
 
 // NW-wave variant for 161..384 rows: the tile is 32 FM rows (FM = 5 or 6) x 32 NW columns, each
@@ -1079,9 +1072,10 @@ static int splits_for(int tiles, int units) {
 }
 
 // The wide 288 x 256 tile where it takes less time than the 288 x 128 one, whole passes of 256
-// workgroups compared with a wide tile measured at 1.8 times a narrow one (137 against 76 us at
-// K = 4096): at 2264 rows gate/up takes 3 wide passes instead of 6 narrow ones, and at 518 one
-// instead of 2, while QKV (2 against 3) and the output and down projections stay narrow.
+// workgroups compared with a wide tile measured at 1.8 times a narrow one (about 132 against
+// 76 us at K = 4096): at 2264 rows gate/up takes 3 wide passes instead of 6 narrow ones, and
+// at 518 one instead of 2, while QKV (2 against 3) and the output and down projections stay
+// narrow.
 // Unsplit only.
 static bool use_wide(int epi, const GemmArgs& a) {
   if (a.splits != 1 || epi == EPI_STORE_F32 || fm_for(a.M) != 9 || a.M <= 32 * 12) return false;
@@ -1092,12 +1086,12 @@ static bool use_wide(int epi, const GemmArgs& a) {
 
 static hipError_t gemm32w_launch(int epi, const GemmArgs& a, hipStream_t s) {
   const int mb = (a.M + 31) / 32, nb = (a.N + 31) / 32;
-  const dim3 grid(((mb + 8) / 9) * ((nb + 7) / 8) * a.splits), block(768);
+  const dim3 grid(((mb + 8) / 9) * ((nb + 7) / 8) * a.splits), block(512);
   switch (epi) {
-    case EPI_STORE: hipLaunchKernelGGL((gemm32w_kernel<9, 3, EPI_STORE>), grid, block, 0, s, a); break;
-    case EPI_RESID: hipLaunchKernelGGL((gemm32w_kernel<9, 3, EPI_RESID>), grid, block, 0, s, a); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((gemm32w_kernel<9, 3, EPI_SWIGLU>), grid, block, 0, s, a); break;
-    case EPI_QKV: hipLaunchKernelGGL((gemm32w_kernel<9, 3, EPI_QKV>), grid, block, 0, s, a); break;
+    case EPI_STORE: hipLaunchKernelGGL((gemm32w_kernel<9, EPI_STORE>), grid, block, 0, s, a); break;
+    case EPI_RESID: hipLaunchKernelGGL((gemm32w_kernel<9, EPI_RESID>), grid, block, 0, s, a); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm32w_kernel<9, EPI_SWIGLU>), grid, block, 0, s, a); break;
+    case EPI_QKV: hipLaunchKernelGGL((gemm32w_kernel<9, EPI_QKV>), grid, block, 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
