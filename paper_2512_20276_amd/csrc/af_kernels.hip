@@ -37,6 +37,29 @@ __global__ __launch_bounds__(NORM_THREADS) void rmsnorm_kernel(const T* __restri
   constexpr int V = 16 / sizeof(T);
   const bool vec = sizeof(T) == 2 && D % 8 == 0 && ldx % 8 == 0;
   float ss = 0.f;
+  if (vec && D <= NORM_THREADS * V) {
+    // at most one chunk per thread: the row and the gain are loaded at once and the row stays in
+    // registers for the normalisation; the same arithmetic, in the same order, as below
+    const int i = threadIdx.x * V;
+    const bool has = i < D;
+    T v[V], gv[V];
+    if (has) {
+      *(uint4*)v = *(const uint4*)(xr + i);
+      *(uint4*)gv = *(const uint4*)(g + i);
+#pragma unroll
+      for (int e = 0; e < V; ++e) ss = fmaf(to_f(v[e]), to_f(v[e]), ss);
+    }
+    const float tot = norm_block_sum(ss, red);
+    const float inv = 1.0f / sqrtf(tot / (float)D + eps);
+    if (has) {
+      T o[V];
+#pragma unroll
+      for (int e = 0; e < V; ++e) o[e] = from_f<T>(to_f(v[e]) * inv * to_f(gv[e]));
+      T* dst = ystride > 0 ? y + frag_off(r_out, i, ystride) : y + (size_t)r_out * ldy + i;
+      *(uint4*)dst = *(const uint4*)o;
+    }
+    return;
+  }
   if (vec) {
     for (int i = threadIdx.x * V; i < D; i += NORM_THREADS * V) {
       T v[V];
@@ -254,6 +277,11 @@ __global__ __launch_bounds__(256) void embed_kernel(const int32_t* __restrict__ 
   else if (id == -1 && embeds) src = embeds + (size_t)m * D;
   if (!src && threadIdx.x == 0) atomicAdd(err_count, 1);
   T* dst = out + (size_t)m * D;
+  constexpr int V = 16 / sizeof(T);
+  if (D % V == 0 && (((uintptr_t)dst | (uintptr_t)src) & 15) == 0) {  // 16-byte chunks
+    for (int i = threadIdx.x * V; i < D; i += 256 * V) *(uint4*)(dst + i) = src ? *(const uint4*)(src + i) : zero4();
+    return;
+  }
   for (int i = threadIdx.x; i < D; i += 256) dst[i] = src ? src[i] : from_f<T>(0.f);
 }
 
