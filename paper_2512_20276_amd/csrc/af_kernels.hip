@@ -93,9 +93,69 @@ __global__ __launch_bounds__(NORM_THREADS) void rmsnorm_kernel(const T* __restri
   }
 }
 
+// Many rows of width D <= 4096 (bf16): one wave per row, eight rows per workgroup.  The gain is
+// loaded once per workgroup into LDS instead of once per row, every chunk of the row is
+// requested before any is used and stays in registers, and no workgroup barrier sits between
+// a row's load and its store.  Lane l holds chunks l + 64 i, which are the chunks thread
+// 64 i + l of rmsnorm_kernel holds; its squares are summed, tree-reduced over the 64 lanes and
+// the eight partial sums added in the same order as there, so every output is bit-identical.
+constexpr int NORM_ROWS_PER_WG = 8;
+__global__ __launch_bounds__(64 * NORM_ROWS_PER_WG) void rmsnorm_rows_kernel(const bf16* __restrict__ x, int ldx,
+                                                                       const int32_t* rows,
+                                                                       const bf16* __restrict__ g, bf16* __restrict__ y,
+                                                                       int ldy, long ystride, int n_rows, int D,
+                                                                       float eps) {
+  constexpr int CPL = NORM_THREADS / 64;  // chunks per lane: 4096 / 8 / 64
+  static_assert(NORM_THREADS == 64 * NORM_ROWS_PER_WG, "one thread of rmsnorm_kernel per chunk");
+  __shared__ __attribute__((aligned(16))) bf16 gs[NORM_THREADS * 8];
+  const int lane = threadIdx.x & 63, r = blockIdx.x * NORM_ROWS_PER_WG + (threadIdx.x >> 6);
+  const int n_chunks = D / 8;
+  if ((int)threadIdx.x < n_chunks) *(uint4*)&gs[8 * threadIdx.x] = *(const uint4*)(g + 8 * threadIdx.x);
+  bf16 v[CPL][8];
+  const bf16* xr = x + (size_t)(r < n_rows ? (rows ? rows[r] : r) : 0) * ldx;
+#pragma unroll
+  for (int i = 0; i < CPL; ++i)
+    if (64 * i + lane < n_chunks && r < n_rows) *(uint4*)v[i] = *(const uint4*)(xr + 8 * (64 * i + lane));
+  float tot = 0.f;
+#pragma unroll
+  for (int i = 0; i < CPL; ++i) {
+    float ss = 0.f;
+    if (64 * i + lane < n_chunks && r < n_rows)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss = fmaf(to_f(v[i][e]), to_f(v[i][e]), ss);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+    tot = i == 0 ? ss : tot + ss;
+  }
+  const float inv = 1.0f / sqrtf(tot / (float)D + eps);
+  __syncthreads();  // the gain is in LDS
+  if (r >= n_rows) return;
+#pragma unroll
+  for (int i = 0; i < CPL; ++i) {
+    const int c = 64 * i + lane;
+    if (c >= n_chunks) continue;
+    bf16 gv[8], o[8];
+    *(uint4*)gv = *(const uint4*)&gs[8 * c];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = from_f<bf16>(to_f(v[i][e]) * inv * to_f(gv[e]));
+    bf16* dst = ystride > 0 ? y + frag_off(r, 8 * c, ystride) : y + (size_t)r * ldy + 8 * c;
+    *(uint4*)dst = *(const uint4*)o;
+  }
+}
+
+// Rows per launch from which the row-per-wave kernel is used (its workgroups then still number
+// 128 or more).
+constexpr int NORM_ROWS_MIN = 1024;
+
 hipError_t launch_rmsnorm(int dtype, const void* x, int ldx, const int32_t* rows, const void* g, void* y, int ldy,
                           long ystride, int n_rows, int D, float eps, hipStream_t s) {
   if (n_rows <= 0) return hipSuccess;
+  if (dtype == AF_BF16 && n_rows >= NORM_ROWS_MIN && D % 8 == 0 && D <= 8 * NORM_THREADS && ldx % 8 == 0) {
+    hipLaunchKernelGGL(rmsnorm_rows_kernel, dim3((n_rows + NORM_ROWS_PER_WG - 1) / NORM_ROWS_PER_WG),
+                       dim3(64 * NORM_ROWS_PER_WG), 0, s, (const bf16*)x, ldx, rows, (const bf16*)g, (bf16*)y, ldy,
+                       ystride, n_rows, D, eps);
+    return hipGetLastError();
+  }
   if (dtype == AF_BF16)
     hipLaunchKernelGGL(rmsnorm_kernel<bf16>, dim3(n_rows), dim3(NORM_THREADS), 0, s, (const bf16*)x, ldx, rows,
                        (const bf16*)g, (bf16*)y, ldy, ystride, D, eps);
