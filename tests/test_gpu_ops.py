@@ -41,7 +41,7 @@ def _assert_close(got, ref, storage, what, min_exact=None, **kw):
 
 # ----------------------------------------------------------------------------- RMSNorm
 @pytest.mark.parametrize("storage", ["bf16", "f32"])
-@pytest.mark.parametrize("M,D", [(1, 256), (34, 256), (282, 4096), (7, 4096)])
+@pytest.mark.parametrize("M,D", [(1, 256), (34, 256), (282, 4096), (7, 4096), (1027, 4096), (2264, 256)])
 def test_rmsnorm(storage, M, D):
     dt = DT[storage]
     x = wl.draw(("t_norm_x", M, D), (M, D), dtype=dt, device="cuda")
@@ -51,6 +51,23 @@ def test_rmsnorm(storage, M, D):
     torch.cuda.synchronize()
     ref = round_storage(rmsnorm(to_np(x), to_np(g), 1e-6), storage)
     _assert_close(y, ref, storage, "rmsnorm", min_exact=0.999, atol=1e-5 if storage == "f32" else 1e-3)
+
+
+@pytest.mark.parametrize("M,D", [(1024, 4096), (2264, 4096), (1031, 256)])
+def test_rmsnorm_many_rows_equals_few_rows(M, D):
+    """From 1024 rows the norm runs one row per wave; every row must equal, bit for bit, the
+    same row normalised in a launch of a few rows (one row per workgroup), including the
+    rows of a last, partly filled workgroup."""
+    x = wl.draw(("t_norm_x", M, D), (M, D), device="cuda")
+    g = wl.draw(("t_norm_g", D), (D,), std=0.3, mean=1.0, device="cuda")
+    y = torch.empty_like(x)
+    af.op_rmsnorm(x, g, y, 1e-6)
+    for r0 in (0, 300, M - 7):
+        part = x[r0:r0 + 7].contiguous()
+        yp = torch.empty_like(part)
+        af.op_rmsnorm(part, g, yp, 1e-6)
+        torch.cuda.synchronize()
+        assert torch.equal(yp, y[r0:r0 + 7]), r0
 
 
 # ----------------------------------------------------------------------------- GEMM core
