@@ -136,8 +136,9 @@ __device__ __forceinline__ void epi_group16(const GemmArgs& a, int m, int c, con
     } else {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        r0[e] = from_f<T>(va[e] * q.cs[2 * e] - vb[e] * q.cs[2 * e + 1]);
-        r1[e] = from_f<T>(vb[e] * q.cs[2 * e] + va[e] * q.cs[2 * e + 1]);
+        // explicit fused multiply-adds: every kernel that applies this epilogue rounds alike
+        r0[e] = from_f<T>(fmaf(va[e], q.cs[2 * e], -(vb[e] * q.cs[2 * e + 1])));
+        r1[e] = from_f<T>(fmaf(vb[e], q.cs[2 * e], va[e] * q.cs[2 * e + 1]));
       }
       dst = q.region == 0 ? (T*)a.out + (size_t)m * a.ldo + q.h * hd
                           : (T*)a.ring_k + (((size_t)q.slot * a.n_heads + q.h) * a.max_pos + q.pos) * hd;
@@ -674,27 +675,33 @@ __global__ __launch_bounds__(256, 1) void gemm32x2_kernel(GemmArgs a) {
   }
 }
 
-// Wide tile for many rows: 32 FM rows x 256 columns on eight waves, each owning one 32-column
-// weight block over all FM row blocks (as gemm32c_kernel does for 160 rows), so no weight
-// fragment is loaded twice.  Per byte loaded into the CU it does 1.5x the MFMA work of the
-// 288 x 128 tile (288 + 256 bytes per row of K for 288 x 256 outputs, against 288 + 128 for
-// 288 x 128).  The accumulators take 16 FM registers; one k step's activation fragments are
-// read at a time (the other wave on the SIMD covers the LDS latency), the weights run two k
-// steps ahead.  Activations by DMA from waves 0..3; the fp32 tile goes through the LDS ring
-// three row blocks per pass.  (Three row groups of four column groups, each wave two weight
-// blocks, measured no faster: each weight fragment was then requested once per row group.)
-template <int FM, int EPI>
-__global__ __launch_bounds__(512, 1) void gemm32w_kernel(GemmArgs a) {
-  constexpr int KS = 4, NBUF = 4, PFB = 2, BLK = 512, NW = 8, TN = 32 * NW, PB = 3;
-  constexpr int SB = FM * KS;        // fragment blocks per stage
-  constexpr int DW = SB / 4;         // DMAs per stage of each of waves 0..3
+// Wide tile for many rows: 32 FM rows x 32 CB NW columns on NW waves, each owning CB 32-column
+// weight blocks over all FM row blocks (as gemm32c_kernel does for 160 rows), so no weight
+// fragment is loaded twice.  Per byte loaded into the CU the 288 x 256 tile does 1.5x the MFMA
+// work of the 288 x 128 one (288 + 256 bytes per row of K for 288 x 256 outputs, against
+// 288 + 128 for 288 x 128).  Every activation fragment read from LDS feeds CB MFMAs: with
+// eight waves of one block each (two waves per SIMD, 144 accumulator registers) the LDS reads
+// of a 16-k step (72 KB) take as long as its MFMAs; with four waves of two blocks (one wave per
+// SIMD, 288 accumulator registers) they take half, and each wave double-buffers its
+// fragments, as no other wave on its SIMD covers the LDS latency.  The weights run two k steps
+// ahead.  Activations by DMA from waves 0..3; the fp32 tile goes through the LDS ring three
+// row blocks per pass.  (Three row groups of four column groups, each wave two weight blocks,
+// measured no faster: each weight fragment was then requested once per row group.  Four
+// waves of two blocks, 256 x 256 with 256 accumulator registers, measured 1.2x slower for
+// gate/up at 2264 rows: one wave per SIMD leaves every wait of a wave on the matrix core.)
+template <int FM, int NW, int CB, int EPI>
+__global__ __launch_bounds__(64 * NW, 1) void gemm32w_kernel(GemmArgs a) {
+  constexpr int KS = 4, NBUF = 4, PFB = 2, BLK = 512, TN = 32 * CB * NW, PB = 3;
+  constexpr int AFB = NW <= 4 ? 2 : 1;  // activation fragment buffers per wave
+  constexpr int SB = FM * KS;           // fragment blocks per stage
+  constexpr int DW = SB / 4;            // DMAs per stage of each of waves 0..3
   constexpr int NPASS = (FM + PB - 1) / PB;
-  static_assert(SB % 4 == 0 && KS % PFB == 0, "pipeline shape");
+  static_assert(SB % 4 == 0 && KS % PFB == 0 && NW >= 4, "pipeline shape");
   __shared__ __attribute__((aligned(1024))) bf16 As[NBUF][SB * BLK];
   static_assert(32 * PB * TN * 4 <= (int)sizeof(As), "an epilogue pass must fit the stage buffers");
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int n_blocks = (a.N + 31) >> 5, n_nt = (n_blocks + NW - 1) / NW;
+  const int n_blocks = (a.N + 31) >> 5, n_nt = (n_blocks + NW * CB - 1) / (NW * CB);
   const int m_blocks = (a.M + 31) >> 5, n_mt = (m_blocks + FM - 1) / FM;
   const int S = a.splits;
   const int t = xcd_remap(blockIdx.x, n_mt * n_nt * S);
@@ -704,8 +711,12 @@ __global__ __launch_bounds__(512, 1) void gemm32w_kernel(GemmArgs a) {
   const int units = ks16 / (KS * NBUF), per = (units + S - 1) / S;
   const int kb = min(units, sp * per) * (KS * NBUF), ke = min(units, sp * per + per) * (KS * NBUF);
   const int n_st = (ke - kb) / KS;  // a multiple of NBUF
-  // this wave's weight block (past N: a valid block whose columns are never stored)
-  const bf16* bp = (const bf16*)a.B + (size_t)min(nt * NW + wave, n_blocks - 1) * a.bstride + lane * 8;
+  // this wave's weight blocks (past N: a valid block whose columns are never stored)
+  const bf16* bp[CB];
+  static_for<0, CB>([&](auto c) {
+    bp[c] = (const bf16*)a.B + (size_t)min((nt * NW + wave) * CB + (int)decltype(c)::value, n_blocks - 1) * a.bstride +
+            lane * 8;
+  });
   const bf16* __restrict__ Ab = (const bf16*)a.A;
   float* T_ = (float*)&As[0][0];
   const int m0 = mt * FM * 32, n0 = nt * TN;
@@ -722,16 +733,18 @@ __global__ __launch_bounds__(512, 1) void gemm32w_kernel(GemmArgs a) {
                                          (__attribute__((address_space(3))) void*)&As[buf][q * BLK], 16, 0, 0);
       });
     };
-    bf16x8 rb[PFB];
+    bf16x8 rb[PFB][CB];
     auto load_b = [&](auto slot, int st, int j) {
       const int k = min(kb + st * KS + j, ks16 - 1);
-      const bf16* src = bp + (size_t)k * BLK;
-      bf16x8 v;
-      asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(src) : "memory");
-      rb[slot] = v;
+      static_for<0, CB>([&](auto c) {
+        const bf16* src = bp[c] + (size_t)k * BLK;
+        bf16x8 v;
+        asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(src) : "memory");
+        rb[slot][c] = v;
+      });
     };
-    f32x16 acc[FM];
-    static_for<0, FM>([&](auto i) { acc[i] = f32x16{}; });
+    f32x16 acc[FM][CB];
+    static_for<0, FM>([&](auto i) { static_for<0, CB>([&](auto c) { acc[i][c] = f32x16{}; }); });
     static_for<0, NBUF - 1>([&](auto b) {
       dma(b, b);
       __builtin_amdgcn_sched_barrier(0);
@@ -744,26 +757,43 @@ __global__ __launch_bounds__(512, 1) void gemm32w_kernel(GemmArgs a) {
         constexpr int U = decltype(u)::value;
         const int st = st0 + U;
         // Loads complete in order.  Stage st's activations come from the DMA at the top of stage
-        // st - NBUF + 1, after which NBUF - 1 stages of weight loads (KS each) and NBUF - 2 DMAs
-        // were issued.  k step j's weights were loaded PFB steps earlier; after them came the
-        // PFB - 1 weight loads of the steps between and, when a stage top lies between, its DMAs.
-        constexpr int WAIT_A = KS * (NBUF - 1) + D * (NBUF - 2);
+        // st - NBUF + 1, after which NBUF - 1 stages of weight loads (CB KS each) and NBUF - 2
+        // DMAs were issued.  k step j's weights were loaded PFB steps earlier; after them came
+        // the CB (PFB - 1) weight loads of the steps between and, when a stage top lies between,
+        // its DMAs.
+        constexpr int WAIT_A = CB * KS * (NBUF - 1) + D * (NBUF - 2);
         static_assert(WAIT_A <= 63, "vmcnt range");
         asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(WAIT_A) : "memory");
         dma(std::integral_constant<int, (U + NBUF - 1) % NBUF>{}, st + NBUF - 1);
         __builtin_amdgcn_sched_barrier(0);
+        bf16x8 af[AFB][FM];
+        if constexpr (AFB == 2) {
+          static_for<0, FM>([&](auto i) {
+            af[0][i] = *(const bf16x8*)(&As[U][((int)decltype(i)::value * KS) * BLK + lane * 8]);
+          });
+        }
         static_for<0, KS>([&](auto j) {
           constexpr int J = decltype(j)::value;
           constexpr int slot = (U * KS + J) % PFB;
-          bf16x8 af[FM];
-          static_for<0, FM>([&](auto i) {
-            af[i] = *(const bf16x8*)(&As[U][((int)decltype(i)::value * KS + J) * BLK + lane * 8]);
-          });
-          constexpr int WAIT_B = (PFB - 1) + (J < PFB ? D : 0);
+          constexpr int CUR = AFB == 2 ? (J & 1) : 0;
+          if constexpr (AFB == 2) {  // the next k step's fragments, read while these MFMAs run
+            if constexpr (J + 1 < KS) {
+              static_for<0, FM>([&](auto i) {
+                af[(J + 1) & 1][i] = *(const bf16x8*)(&As[U][((int)decltype(i)::value * KS + J + 1) * BLK + lane * 8]);
+              });
+            }
+          } else {
+            static_for<0, FM>([&](auto i) {
+              af[0][i] = *(const bf16x8*)(&As[U][((int)decltype(i)::value * KS + J) * BLK + lane * 8]);
+            });
+          }
+          constexpr int WAIT_B = CB * (PFB - 1) + (J < PFB ? D : 0);
           asm volatile("s_waitcnt vmcnt(%0)" ::"n"(WAIT_B) : "memory");
           __builtin_amdgcn_sched_barrier(0);
           static_for<0, FM>([&](auto i) {
-            acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], rb[slot], acc[i], 0, 0, 0);
+            static_for<0, CB>([&](auto c) {
+              acc[i][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[CUR][i], rb[slot][c], acc[i][c], 0, 0, 0);
+            });
           });
           load_b(std::integral_constant<int, slot>{}, st + (J + PFB) / KS, (J + PFB) % KS);
           __builtin_amdgcn_sched_barrier(0);
@@ -773,7 +803,9 @@ __global__ __launch_bounds__(512, 1) void gemm32w_kernel(GemmArgs a) {
     // the ring's last (unused) loads land before any of its registers can be reused
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 #pragma unroll
-    for (int p = 0; p < PFB; ++p) asm volatile("" : "+v"(rb[p]));
+    for (int p = 0; p < PFB; ++p)
+#pragma unroll
+      for (int c = 0; c < CB; ++c) asm volatile("" : "+v"(rb[p][c]));
 
     // ---- epilogue, PB row blocks per pass through the stage buffers
     constexpr bool paired = EPI == EPI_SWIGLU || EPI == EPI_QKV;
@@ -783,10 +815,13 @@ __global__ __launch_bounds__(512, 1) void gemm32w_kernel(GemmArgs a) {
       constexpr int NB = PS * PB + PB <= FM ? PB : FM - PS * PB;  // row blocks in this pass
       __syncthreads();  // every wave's DMAs have landed and the buffers' last readers are done
       static_for<0, NB>([&](auto i) {
-        static_for<0, 16>([&](auto r) {
-          constexpr int R = decltype(r)::value;
-          const int row = (int)decltype(i)::value * 32 + 8 * (R / 4) + 4 * (lane >> 5) + (R % 4);
-          T_[row * TN + wave * 32 + (lane & 31)] = acc[PS * PB + decltype(i)::value][R];
+        static_for<0, CB>([&](auto c) {
+          static_for<0, 16>([&](auto r) {
+            constexpr int R = decltype(r)::value;
+            const int row = (int)decltype(i)::value * 32 + 8 * (R / 4) + 4 * (lane >> 5) + (R % 4);
+            T_[row * TN + (wave * CB + (int)decltype(c)::value) * 32 + (lane & 31)] =
+                acc[PS * PB + decltype(i)::value][decltype(c)::value][R];
+          });
         });
       });
       __syncthreads();
@@ -1086,12 +1121,13 @@ static bool use_wide(int epi, const GemmArgs& a) {
 
 static hipError_t gemm32w_launch(int epi, const GemmArgs& a, hipStream_t s) {
   const int mb = (a.M + 31) / 32, nb = (a.N + 31) / 32;
-  const dim3 grid(((mb + 8) / 9) * ((nb + 7) / 8) * a.splits), block(512);
+  constexpr int FM = 9, NW = 8, CB = 1;
+  const dim3 grid(((mb + FM - 1) / FM) * ((nb + NW * CB - 1) / (NW * CB)) * a.splits), block(64 * NW);
   switch (epi) {
-    case EPI_STORE: hipLaunchKernelGGL((gemm32w_kernel<9, EPI_STORE>), grid, block, 0, s, a); break;
-    case EPI_RESID: hipLaunchKernelGGL((gemm32w_kernel<9, EPI_RESID>), grid, block, 0, s, a); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((gemm32w_kernel<9, EPI_SWIGLU>), grid, block, 0, s, a); break;
-    case EPI_QKV: hipLaunchKernelGGL((gemm32w_kernel<9, EPI_QKV>), grid, block, 0, s, a); break;
+    case EPI_STORE: hipLaunchKernelGGL((gemm32w_kernel<FM, NW, CB, EPI_STORE>), grid, block, 0, s, a); break;
+    case EPI_RESID: hipLaunchKernelGGL((gemm32w_kernel<FM, NW, CB, EPI_RESID>), grid, block, 0, s, a); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm32w_kernel<FM, NW, CB, EPI_SWIGLU>), grid, block, 0, s, a); break;
+    case EPI_QKV: hipLaunchKernelGGL((gemm32w_kernel<FM, NW, CB, EPI_QKV>), grid, block, 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
