@@ -450,13 +450,14 @@ def test_7b_32_layer_packed_equals_sequential_on_gpu(split_k):
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("K,L_T", [(16, 20), (24, 64), (32, 20)])
+@pytest.mark.parametrize("K,L_T", [(16, 20), (24, 64), (32, 20), (7, 256)])
 def test_7b_k_sweep_packed_equals_sequential_4_layers(K, L_T):
-    """The K sweep's points beyond K = 7 (a prefill of 256 vision rows and L_T instruction rows
-    packed with K - 1 decode rows; at K = 24 and 32 the decode rows take their own attention
-    launch; K = 24 with the 64-row instruction of a longer prefill): with split-K off every row,
-    logit and token of requests 0 and 1 equals the plain per-request run on the same kernels,
-    bit for bit (a 4-layer model of the 7B shape)."""
+    """The K sweep's points beyond the benchmark's (a prefill of 256 vision rows and L_T
+    instruction rows packed with K - 1 decode rows; at K = 24 and 32 the decode rows take their
+    own attention launch; K = 24 with the 64-row instruction of a longer prefill, 326..343 rows
+    on 192-row tiles; L_T = 256, 518 rows, gate/up on the 288 x 256 tile): with split-K off
+    every row, logit and token of requests 0 and 1 equals the plain per-request run on the same
+    kernels, bit for bit (a 4-layer model of the 7B shape)."""
     shape = wl.LLAMA7B.with_layers(4)
     L_V = 256
     L_P, D, V = L_V + L_T, shape.d_model, shape.vocab
