@@ -28,6 +28,7 @@ namespace af {
 // split order (deterministic) before the epilogue.
 template <typename T, int EPI>
 __device__ __forceinline__ void epi_single(const GemmArgs& a, int m, int n, float v) {
+  n += a.col0;
   if constexpr (EPI == EPI_STORE) {
     ((T*)a.out)[(size_t)m * a.ldo + n] = from_f<T>(v);
   } else if constexpr (EPI == EPI_STORE_F32) {
@@ -42,6 +43,7 @@ __device__ __forceinline__ void epi_single(const GemmArgs& a, int m, int n, floa
 // (weights repacked that way); c is the a-column, va/vb the pair.
 template <typename T, int EPI>
 __device__ __forceinline__ void epi_pair(const GemmArgs& a, int m, int c, float va, float vb) {
+  c += a.col0;
   if constexpr (EPI == EPI_SWIGLU) {
     const int f = (c >> 4) * 8 + (c & 7);
     const float s = va / (1.0f + __expf(-va));
@@ -60,7 +62,7 @@ __device__ __forceinline__ void epi_pair(const GemmArgs& a, int m, int c, float 
     } else {
       const float cs = a.rope_cs[((size_t)pos * half + dj) * 2];
       const float sn = a.rope_cs[((size_t)pos * half + dj) * 2 + 1];
-      const float ra = va * cs - vb * sn, rb = vb * cs + va * sn;
+      const float ra = fmaf(va, cs, -(vb * sn)), rb = fmaf(vb, cs, va * sn);  // as epi_group16
       T* dst = region == 0 ? (T*)a.out + (size_t)m * a.ldo + h * hd
                            : (T*)a.ring_k + (((size_t)slot * a.n_heads + h) * a.max_pos + pos) * hd;
       dst[dj] = from_f<T>(ra);
@@ -72,6 +74,7 @@ __device__ __forceinline__ void epi_pair(const GemmArgs& a, int m, int c, float 
 // Columns nc .. nc+7 (nc % 8 == 0) of row m.
 template <typename T, int EPI>
 __device__ __forceinline__ void epi_group8(const GemmArgs& a, int m, int nc, const float* v) {
+  nc += a.col0;
   if constexpr (EPI == EPI_STORE_F32) {
     store8<float>((float*)a.out + (size_t)m * a.ldo + nc, v);
   } else {
@@ -97,6 +100,7 @@ struct QkvRow {
   float cs[16];
   __device__ __forceinline__ void load(const GemmArgs& a, int m, int c) {
     const int D = a.d_model, hd = a.head_dim, half = hd >> 1;
+    c += a.col0;
     region = c / D;
     const int cr = c - region * D;
     h = cr / hd;
@@ -116,7 +120,7 @@ __device__ __forceinline__ void epi_group16(const GemmArgs& a, int m, int c, con
                                             const QkvRow* pre = nullptr) {
   T r0[8], r1[8];
   if constexpr (EPI == EPI_SWIGLU) {
-    const int f = (c >> 4) * 8;
+    const int f = ((c + a.col0) >> 4) * 8;
 #pragma unroll
     for (int e = 0; e < 8; ++e) r0[e] = from_f<T>(va[e] / (1.0f + __expf(-va[e])) * vb[e]);
     store8<T>((T*)a.out + (a.ostride > 0 ? frag_off(m, f, a.ostride) : (size_t)m * a.ldo + f), r0);
@@ -1109,14 +1113,21 @@ static int splits_for(int tiles, int units) {
 // The wide 288 x 256 tile where it takes less time than the 288 x 128 one, whole passes of 256
 // workgroups compared with a wide tile measured at 1.8 times a narrow one (about 132 against
 // 76 us at K = 4096): at 2264 rows gate/up takes 3 wide passes instead of 6 narrow ones, and
-// at 518 one instead of 2, while QKV (2 against 3) and the output and down projections stay
-// narrow.
-// Unsplit only.
-static bool use_wide(int epi, const GemmArgs& a) {
-  if (a.splits != 1 || epi == EPI_STORE_F32 || fm_for(a.M) != 9 || a.M <= 32 * 12) return false;
+// at 518 one instead of 2.  Where one pass of wide tiles over the first columns and narrow
+// tiles for the rest cost less than either alone (QKV at 2264 rows: 1 wide pass over 8192
+// columns and 1 narrow pass over 4096, against 3 narrow or 2 wide passes), the launch is split
+// there.  The output and down projections at 2264 rows stay narrow.  Unsplit only.
+// Returns 0 (narrow), 1 (wide) or the first narrow column of a split launch.
+static int wide_plan(int epi, const GemmArgs& a) {
+  if (a.splits != 1 || a.col0 != 0 || epi == EPI_STORE_F32 || fm_for(a.M) != 9 || a.M <= 32 * 12) return 0;
   const int mb = (a.M + 31) / 32, nb = (a.N + 31) / 32, n_mt = (mb + 8) / 9;
-  const long tw = (long)n_mt * ((nb + 7) / 8), tn = (long)n_mt * ((nb + 3) / 4);
-  return ((tw + 255) / 256) * 18 < ((tn + 255) / 256) * 10;
+  auto passes = [](long t) { return (t + 255) / 256; };
+  const long cost_n = passes((long)n_mt * ((nb + 3) / 4)) * 10;
+  const long cost_w = passes((long)n_mt * ((nb + 7) / 8)) * 18;
+  const int wblocks = (256 / n_mt) * 8;  // column blocks of one pass of wide tiles
+  const long cost_h = wblocks > 0 && wblocks < nb ? 18 + passes((long)n_mt * ((nb - wblocks + 3) / 4)) * 10 : cost_w + 1;
+  if (cost_h < cost_w && cost_h < cost_n) return wblocks * 32;
+  return cost_w < cost_n ? 1 : 0;
 }
 
 static hipError_t gemm32w_launch(int epi, const GemmArgs& a, hipStream_t s) {
@@ -1142,7 +1153,18 @@ static hipError_t gemm_dispatch_bf16(int epi, const GemmArgs& a, hipStream_t s) 
     if (e != hipSuccess || a.splits <= 1 || a.partials_only) return e;
     return reduce_launch<bf16>(epi, a, s);
   }
-  if (use_wide(epi, a)) return gemm32w_launch(epi, a, s);
+  if (const int plan = wide_plan(epi, a)) {
+    if (plan == 1) return gemm32w_launch(epi, a, s);
+    // columns [0, plan) on wide tiles, the rest on 288 x 128 tiles
+    GemmArgs aw = a, an = a;
+    aw.N = plan;
+    an.N = a.N - plan;
+    an.col0 = plan;
+    an.B = (const bf16*)a.B + (size_t)(plan / 32) * a.bstride;
+    e = gemm32w_launch(epi, aw, s);
+    if (e != hipSuccess) return e;
+    return gemm32_launch<9, true>(epi, an, s);
+  }
   switch (fm_for(a.M)) {
     case 1: e = gemm32_launch<1, false>(epi, a, s); break;
     case 3: e = gemm32_launch<3, true>(epi, a, s); break;

@@ -54,6 +54,7 @@ struct GemmArgs {
   int splits;      // split-K factor (1 = none)
   float* partial;  // [splits][M][N] fp32 partial sums when splits > 1
   int partials_only;  // with splits > 1: leave the sums and the epilogue to a later kernel
+  int col0;        // first column of this launch in the full output (a launch over a column range; unsplit)
   void* out;       // EPI_STORE/_F32/_RESID: [M, N]; EPI_SWIGLU: [M, N/2]; EPI_QKV: queries [M, d_model]
   int ldo;
   long ostride;    // EPI_SWIGLU: > 0 writes the output fragment-tiled (32-row blocks ostride apart)

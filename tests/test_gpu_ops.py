@@ -132,11 +132,11 @@ def test_linear_large_m():
     _assert_close(y, ref, "bf16", "linear", min_exact=0.99, atol=1e-3, rtol=8e-3)
 
 
-@pytest.mark.parametrize("M,N", [(400, 22016), (2264, 4672)])
-def test_linear_wide_tile(M, N):
+@pytest.mark.parametrize("M,N,K", [(400, 22016, 4096), (2264, 4672, 4096), (2264, 12288, 512)])
+def test_linear_wide_tile(M, N, K):
     """Shapes that take the 288 x 256 tile (two row tiles of gate/up width; eight row tiles with
-    a last column tile half past N), against fp64."""
-    K = 4096
+    a last column tile half past N; QKV width at 2264 rows, one pass of wide tiles over the
+    first 8192 columns and 288 x 128 tiles for the rest), against fp64."""
     x = wl.draw(("t_lin_x", M, K), (M, K), device="cuda")
     w = wl.draw(("t_lin_w", N, K), (N, K), std=0.02, device="cuda")
     y = torch.full((M, N), float("nan"), dtype=torch.bfloat16, device="cuda")
