@@ -200,16 +200,17 @@ def _logits_report(got, ref):
 
 
 @pytest.mark.timeout(1200)
-@pytest.mark.parametrize("K", [7, 16])
+@pytest.mark.parametrize("K", [7, 16, 32])
 def test_7b_32_layer_pipeline_matches_oracle(monkeypatch, K):
-    """The benchmark workload (32 layers, K = 7, 8 slots) and the K sweep's K = 16 point (17
-    slots) against the oracle pipeline.
+    """The benchmark workload (32 layers, K = 7, 8 slots) and the K sweep's K = 16 and K = 32
+    points (K + 1 slots; at K = 32 the 31 decode rows take their own attention launch beside the
+    query tiles) against the oracle pipeline.
 
     The GPU pipeline runs steps 0..K-1 on its own greedy tokens; the oracle pipeline (Alg. 1
     over the float64 packed forward with bf16 storage) runs the same steps forced with the
     GPU's tokens, so the two trajectories never part.  Step K-1 is the first full step: a
     276-row prefill and K-1 decode rows at contexts 277..276+K-1 (M = 282 at K = 7, 291 at
-    K = 16).
+    K = 16, 307 at K = 32).
       * Per layer (the gate): each of the 32 layers of step K-1 runs on the GPU from the
         oracle's input to that layer, with the oracle's ring history of that layer, and is held
         to the layer gate (max-abs 2e-2 / rel 1e-2 elementwise, normwise and per row).
