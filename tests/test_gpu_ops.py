@@ -167,6 +167,10 @@ ATTN_CASES = {
     "mixed_7b_step": [(10, 0, 276)] + [(10 - s, 276 + s - 1, 1) for s in range(1, 7)],
     "chunked_prefill": [(1, 100, 70), (2, 0, 1), (3, 5, 64), (4, 200, 1)],
     "single_key": [(1, 0, 1)],
+    # the ring's last position (max_pos = 288): a decode row at 287 and a prefill ending there
+    "ring_end": [(1, 287, 1), (2, 200, 88), (3, 255, 1)],
+    # query-tile and key-chunk edges: 64 and 65 prefill rows, decode rows at 31, 32, 64, 95
+    "tile_edges": [(1, 0, 64), (2, 0, 65), (3, 31, 1), (4, 32, 1), (5, 64, 1), (6, 95, 1)],
     # more than 16 decode rows beside a prefill at 32 heads: the query tiles and the decode
     # rows take two launches (the K = 32 step of the K sweep, and the stress step's mix)
     "k32_step": [(40, 0, 276)] + [(40 - s, 276 + s - 1, 1) for s in range(1, 32)],
