@@ -160,7 +160,7 @@ __device__ __forceinline__ void attention_decode_rows(const AttnArgs& a, int fir
 }
 
 // Query tiles of multi-row segments.  The next key/value tile is loaded into registers while
-// the current one is processed from LDS (one memory latency per segment, not per tile).
+// the current one is processed from LDS (its load overlaps the current tile's arithmetic).
 // The segment's key tiles are split between two key groups (group g takes tiles g, g + 2,
 // g + 4, ..), each with a softmax state of its own, and group 1's state is merged into group
 // 0's at the end.  With NWG = 8 waves the two groups run at once, four waves each, with LDS
