@@ -13,6 +13,7 @@ Greedy tokens are compared exactly wherever the oracle's top-2 margin exceeds tw
 largest logit deviation of that row, capped at 0.05; rows inside that window are near-ties.
 """
 import math
+import os
 
 import numpy as np
 import pytest
@@ -200,7 +201,9 @@ def _logits_report(got, ref):
 
 
 @pytest.mark.timeout(1200)
-@pytest.mark.parametrize("K", [7, 16, 32])
+@pytest.mark.parametrize("K", [7, 16, pytest.param(32, marks=pytest.mark.skipif(
+    os.environ.get("AF_LONG_TESTS") != "1",
+    reason="32 oracle pipeline steps take about 200 s with no output; set AF_LONG_TESTS=1 to run"))])
 def test_7b_32_layer_pipeline_matches_oracle(monkeypatch, K):
     """The benchmark workload (32 layers, K = 7, 8 slots) and the K sweep's K = 16 and K = 32
     points (K + 1 slots; at K = 32 the 31 decode rows take their own attention launch beside the
