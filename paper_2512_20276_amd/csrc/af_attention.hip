@@ -46,7 +46,7 @@ __device__ __forceinline__ float dot_vec(const uint4& k, const uint4& q, float a
 // waves runs two of them one after the other) merged in virtual-wave order, so the result does
 // not depend on how many rows share the workgroup or how many waves it has.
 template <typename T, int HD, int ROWS, int NWG = ATTN_WAVES>
-__device__ __forceinline__ void attention_decode_rows(const AttnArgs& a, int first) {
+__device__ __forceinline__ void attention_decode_rows(const AttnArgs& a, int first, int h) {
   constexpr int VEC = Chunk<T>::N;  // elements per 16 bytes
   constexpr int DG = HD / VEC;      // 16-byte chunks per key row
   constexpr int KH2 = DG / 2;       // chunks per half row (two lanes per key for the scores)
@@ -64,7 +64,6 @@ __device__ __forceinline__ void attention_decode_rows(const AttnArgs& a, int fir
   const int sub = ROWS == 1 ? 0 : wave0 / NW, wave = ROWS == 1 ? wave0 : wave0 % NW;  // row, wave within it
   const bool live = ROWS == 1 || first + sub < a.n_tiles;  // an odd count leaves the last half idle
   const int seg_i = a.tiles[2 * (live ? first + sub : first)];
-  const int h = blockIdx.y;
   const DevSeg sg = a.segs[seg_i];
   const int kv_len = live ? sg.pos0 + 1 : 0;
   const size_t slot_off = ((size_t)sg.slot * a.n_heads + h) * a.max_pos * HD;
@@ -190,7 +189,7 @@ __device__ __forceinline__ void merge_state(float& m0, float& l0, float m1, floa
 }
 
 template <typename T, int HD, int NWG>
-__device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int tile, char* smem) {
+__device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int tile, int h, char* smem) {
   typedef AttnLds<T, HD> L;
   constexpr int VEC = L::VEC, KROW = L::KROW, VROW = L::VROW;
   constexpr int KST = HD / 32;              // MFMA k steps over the head dimension
@@ -207,7 +206,6 @@ __device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int ti
   T* const Vt = Ks + L::K_ELEMS;
   const int lr = lane & 15, lg = lane >> 4;
   const int seg_i = a.tiles[2 * tile], i0 = a.tiles[2 * tile + 1];
-  const int h = blockIdx.y;
   const DevSeg sg = a.segs[seg_i];
   const int rows_here = min(ATTN_BQ, sg.q_len - i0);
   const int kv_end = sg.pos0 + i0 + rows_here;  // exclusive: keys this tile can see
@@ -443,21 +441,24 @@ __device__ __forceinline__ void attention_prefill_tile(const AttnArgs& a, int ti
 }
 
 // One launch for the whole step: work tiles [0, n_multi) are query tiles of multi-row segments
-// (ordered longest first, so they start first), the rest single-row segments.
-// Blocks [0, n_multi) of the query-tile instance take the query tiles, its other blocks pairs of
-// single-row tiles (n_multi + 2 (blockIdx.x - n_multi) and the next); the decode-only instance
-// takes one single-row tile per block (n_multi + blockIdx.x), on all of its waves.
+// (ordered longest first), the rest single-row segments.  The grid is one-dimensional with the
+// head varying fastest, block = item * n_heads + head: every head of the longest query tile is
+// dispatched first and the short items last, and the query tiles of one head (32 blocks apart
+// at 32 heads) land on the same XCD, whose L2 then serves the segment's keys to all of them.
+// Items [0, n_multi) of the query-tile instance are the query tiles, its other items pairs of
+// single-row tiles (n_multi + 2 (item - n_multi) and the next); the decode-only instance takes
+// one single-row tile per item (n_multi + item), on all of its waves.
 template <typename T, int HD, bool PREFILL>
 __global__ __launch_bounds__(64 * ATTN_WAVES, !PREFILL ? 4 : 2) void attention_kernel(AttnArgs a) {
-  const int b = blockIdx.x;
+  const int b = blockIdx.x / a.n_heads, h = blockIdx.x % a.n_heads;
   if constexpr (PREFILL) {
     __shared__ __attribute__((aligned(16))) char smem[AttnLds<T, HD>::bytes(8)];
     if (b < a.n_multi)
-      attention_prefill_tile<T, HD, 8>(a, b, smem);
+      attention_prefill_tile<T, HD, 8>(a, b, h, smem);
     else
-      attention_decode_rows<T, HD, 2>(a, a.n_multi + 2 * (b - a.n_multi));
+      attention_decode_rows<T, HD, 2>(a, a.n_multi + 2 * (b - a.n_multi), h);
   } else {
-    attention_decode_rows<T, HD, 1>(a, a.n_multi + b);
+    attention_decode_rows<T, HD, 1>(a, a.n_multi + b, h);
   }
 }
 
@@ -468,12 +469,12 @@ __global__ __launch_bounds__(64 * ATTN_WAVES, !PREFILL ? 4 : 2) void attention_k
 // work; the results are those of the eight-wave instances bit for bit.
 template <typename T, int HD>
 __global__ __launch_bounds__(256, 3) void attention_kernel4(AttnArgs a) {
-  const int b = blockIdx.x;
+  const int b = blockIdx.x / a.n_heads, h = blockIdx.x % a.n_heads;  // head fastest, as above
   __shared__ __attribute__((aligned(16))) char smem[AttnLds<T, HD>::bytes(4)];
   if (b < a.n_multi)
-    attention_prefill_tile<T, HD, 4>(a, b, smem);
+    attention_prefill_tile<T, HD, 4>(a, b, h, smem);
   else
-    attention_decode_rows<T, HD, 1, 4>(a, b);
+    attention_decode_rows<T, HD, 1, 4>(a, b, h);
 }
 
 // Query tiles and decode rows share one launch, query tiles first: eight-wave workgroups (two
@@ -489,11 +490,11 @@ static void attention_launch(const AttnArgs& a0, int n_tiles, hipStream_t s) {
   const dim3 block(64 * ATTN_WAVES);
   const int n_single = n_tiles - a.n_multi, n_pairs = (n_single + 1) / 2;
   if (a.n_multi == 0) {
-    hipLaunchKernelGGL((attention_kernel<T, HD, false>), dim3(n_tiles, a.n_heads), block, 0, s, a);
+    hipLaunchKernelGGL((attention_kernel<T, HD, false>), dim3(n_tiles * a.n_heads), block, 0, s, a);
   } else if ((long)n_pairs * a.n_heads <= 256) {
-    hipLaunchKernelGGL((attention_kernel<T, HD, true>), dim3(a.n_multi + n_pairs, a.n_heads), block, 0, s, a);
+    hipLaunchKernelGGL((attention_kernel<T, HD, true>), dim3((a.n_multi + n_pairs) * a.n_heads), block, 0, s, a);
   } else {
-    hipLaunchKernelGGL((attention_kernel4<T, HD>), dim3(n_tiles, a.n_heads), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((attention_kernel4<T, HD>), dim3(n_tiles * a.n_heads), dim3(256), 0, s, a);
   }
 }
 
