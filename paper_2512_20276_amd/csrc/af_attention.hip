@@ -463,13 +463,27 @@ __global__ __launch_bounds__(64 * ATTN_WAVES, !PREFILL ? 4 : 2) void attention_k
 }
 
 // Four-wave workgroups for steps whose decode rows would more than fill the GPU beside the query
-// tiles (many pipelines, long action chunks): block b < n_multi takes query tile b
-// (its key groups one after the other), any other block the single-row tile b.  Several such
-// workgroups share a CU, so the decode rows' key and value streams overlap the query tiles'
-// work; the results are those of the eight-wave instances bit for bit.
+// tiles (many pipelines, long action chunks): work item b < n_multi is query tile b (its key
+// groups one after the other), any other the single-row tile b.  Several such workgroups share
+// a CU, and the blocks alternate between the two kinds in groups of eight (one block per XCD
+// each), so the decode rows' key and value streams run beside the latency-bound query tiles from
+// the start instead of after them.  Within each kind the order is (work item, head) with the
+// head fastest, so a query tile's XCD is still set by its head.  The results are those of the
+// eight-wave instances bit for bit.
 template <typename T, int HD>
 __global__ __launch_bounds__(256, 3) void attention_kernel4(AttnArgs a) {
-  const int b = blockIdx.x / a.n_heads, h = blockIdx.x % a.n_heads;  // head fastest, as above
+  const int nb_t = a.n_multi * a.n_heads, nb_d = (a.n_tiles - a.n_multi) * a.n_heads;
+  const int inter = min(nb_t, nb_d) / 8 * 8;  // blocks of each kind that alternate
+  const int x = blockIdx.x;
+  int item;  // (work item) * n_heads + head
+  if (x < 2 * inter) {
+    const int g = x >> 4, r = x & 15;
+    item = r < 8 ? g * 8 + r : nb_t + g * 8 + (r - 8);
+  } else {  // the rest: query tiles left over, then decode rows
+    const int rest = x - 2 * inter, t_left = nb_t - inter;
+    item = rest < t_left ? inter + rest : nb_t + inter + (rest - t_left);
+  }
+  const int b = item / a.n_heads, h = item % a.n_heads;
   __shared__ __attribute__((aligned(16))) char smem[AttnLds<T, HD>::bytes(4)];
   if (b < a.n_multi)
     attention_prefill_tile<T, HD, 4>(a, b, h, smem);
