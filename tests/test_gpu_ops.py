@@ -176,9 +176,13 @@ ATTN_CASES = {
     "k32_step": [(40, 0, 276)] + [(40 - s, 276 + s - 1, 1) for s in range(1, 32)],
     "stress_mix": [(1000 + p, 0, 276) for p in range(8)] +
                   [(1000 + 8 * s + p, 276 + s - 1, 1) for s in range(1, 8) for p in range(8)],
+    # four prefills beside 17 decode rows: the four-wave launch, with more query-tile blocks
+    # (640) than decode blocks (544), so query tiles are left over once the two kinds stop
+    # alternating
+    "tiles_exceed_decode": [(2000 + p, 0, 276) for p in range(4)] + [(2100 + i, 100 + 10 * i, 1) for i in range(17)],
 }
 # cases that need a larger ring than 8 slots x 288, and run only at 32 heads x 128
-ATTN_RING = {"k32_step": (33, 320), "stress_mix": (64, 288)}
+ATTN_RING = {"k32_step": (33, 320), "stress_mix": (64, 288), "tiles_exceed_decode": (24, 288)}
 
 
 @pytest.mark.parametrize("storage,H,hd", [("bf16", 32, 128), ("bf16", 4, 64), ("f32", 4, 64), ("f32", 2, 128)])
