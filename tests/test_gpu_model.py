@@ -206,8 +206,8 @@ def _logits_report(got, ref):
     reason="32 oracle pipeline steps take about 200 s with no output; set AF_LONG_TESTS=1 to run"))])
 def test_7b_32_layer_pipeline_matches_oracle(monkeypatch, K):
     """The benchmark workload (32 layers, K = 7, 8 slots) and the K sweep's K = 16 and K = 32
-    points (K + 1 slots; at K = 32 the 31 decode rows take their own attention launch beside the
-    query tiles) against the oracle pipeline.
+    points (K + 1 slots; at K = 32 the 31 decode rows and the query tiles take the four-wave
+    attention launch) against the oracle pipeline.
 
     The GPU pipeline runs steps 0..K-1 on its own greedy tokens; the oracle pipeline (Alg. 1
     over the float64 packed forward with bf16 storage) runs the same steps forced with the
@@ -457,8 +457,9 @@ def test_7b_32_layer_packed_equals_sequential_on_gpu(split_k):
 @pytest.mark.parametrize("K,L_T", [(16, 20), (24, 64), (32, 20), (7, 256)])
 def test_7b_k_sweep_packed_equals_sequential_4_layers(K, L_T):
     """The K sweep's points beyond the benchmark's (a prefill of 256 vision rows and L_T
-    instruction rows packed with K - 1 decode rows; at K = 24 and 32 the decode rows take their
-    own attention launch; K = 24 with the 64-row instruction of a longer prefill, 326..343 rows
+    instruction rows packed with K - 1 decode rows; at K = 24 and 32 the decode rows and the
+    query tiles take the four-wave attention launch; K = 24 with the 64-row instruction of a
+    longer prefill, 326..343 rows
     on 192-row tiles; L_T = 256, 518 rows, gate/up on the 288 x 256 tile): with split-K off
     every row, logit and token of requests 0 and 1 equals the plain per-request run on the same
     kernels, bit for bit (a 4-layer model of the 7B shape)."""

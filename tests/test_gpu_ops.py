@@ -172,7 +172,8 @@ ATTN_CASES = {
     # query-tile and key-chunk edges: 64 and 65 prefill rows, decode rows at 31, 32, 64, 95
     "tile_edges": [(1, 0, 64), (2, 0, 65), (3, 31, 1), (4, 32, 1), (5, 64, 1), (6, 95, 1)],
     # more than 16 decode rows beside a prefill at 32 heads: the query tiles and the decode
-    # rows take two launches (the K = 32 step of the K sweep, and the stress step's mix)
+    # rows take one launch of four-wave workgroups (the K = 32 step of the K sweep, and the
+    # stress step's mix)
     "k32_step": [(40, 0, 276)] + [(40 - s, 276 + s - 1, 1) for s in range(1, 32)],
     "stress_mix": [(1000 + p, 0, 276) for p in range(8)] +
                   [(1000 + 8 * s + p, 276 + s - 1, 1) for s in range(1, 8) for p in range(8)],
@@ -191,7 +192,7 @@ def test_attention(storage, H, hd, case):
     dt = DT[storage]
     n_slots, max_pos = ATTN_RING.get(case, (8, 288))
     if case in ATTN_RING and (storage, H, hd) != ("bf16", 32, 128):
-        pytest.skip("two-launch cases run at the 7B head shape")
+        pytest.skip("four-wave launch cases run at the 7B head shape")
     ring = af.Ring(1, n_slots, max_pos, H, hd, dtype=dt)
     advance_head(ring, 3)  # start the rotation mid-ring so slots wrap
     K, V = _fill_ring(ring, 0, n_slots, max_pos, H, hd, dt, ("t_attn", storage, H, hd))
