@@ -491,10 +491,10 @@ __global__ __launch_bounds__(256, 3) void attention_kernel4(AttnArgs a) {
     attention_decode_rows<T, HD, 1, 4>(a, b, h);
 }
 
-// Query tiles and decode rows share one launch, query tiles first: eight-wave workgroups (two
-// decode rows each) while the decode rows fit one pass over the CUs, else four-wave workgroups
-// (one decode row each), two of which share a CU; a step without query tiles takes the
-// decode-only instance.  Where the decode rows are many, overlapping their key and value
+// Query tiles and decode rows share one launch: eight-wave workgroups (two decode rows each,
+// after the query tiles) while the decode rows fit one pass over the CUs, else four-wave
+// workgroups (one decode row each, alternating with the query tiles), two of which share a CU;
+// a step without query tiles takes the decode-only instance.  Where the decode rows are many, overlapping their key and value
 // streams with the query tiles pays more than the query tiles' own two concurrent key groups
 // (measured on the 8-pipeline step); where they are few, the query tiles' latency decides.
 template <typename T, int HD>
