@@ -492,11 +492,13 @@ __global__ __launch_bounds__(256, 3) void attention_kernel4(AttnArgs a) {
 }
 
 // Query tiles and decode rows share one launch: eight-wave workgroups (two decode rows each,
-// after the query tiles) while the decode rows fit one pass over the CUs, else four-wave
-// workgroups (one decode row each, alternating with the query tiles), two of which share a CU;
-// a step without query tiles takes the decode-only instance.  Where the decode rows are many, overlapping their key and value
-// streams with the query tiles pays more than the query tiles' own two concurrent key groups
-// (measured on the 8-pipeline step); where they are few, the query tiles' latency decides.
+// after the query tiles) while the decode rows fit one pass over the CUs and the whole launch
+// fits 1.4 passes, else four-wave workgroups (one decode row each, alternating with the query
+// tiles), two of which share a CU; a step without query tiles takes the decode-only instance.
+// Where the decode rows are many, overlapping their key and value streams with the query tiles
+// pays more than the query tiles' own two concurrent key groups (measured on the 8-pipeline
+// step, and on a 276- or 512-row prefill beside 7 to 15 decode rows); just past one pass the
+// eight-wave launch's second pass is short and the query tiles' latency decides.
 template <typename T, int HD>
 static void attention_launch(const AttnArgs& a0, int n_tiles, hipStream_t s) {
   AttnArgs a = a0;
@@ -505,7 +507,7 @@ static void attention_launch(const AttnArgs& a0, int n_tiles, hipStream_t s) {
   const int n_single = n_tiles - a.n_multi, n_pairs = (n_single + 1) / 2;
   if (a.n_multi == 0) {
     hipLaunchKernelGGL((attention_kernel<T, HD, false>), dim3(n_tiles * a.n_heads), block, 0, s, a);
-  } else if ((long)n_pairs * a.n_heads <= 256) {
+  } else if ((long)n_pairs * a.n_heads <= 256 && (long)(a.n_multi + n_pairs) * a.n_heads * 5 <= 256 * 7) {
     hipLaunchKernelGGL((attention_kernel<T, HD, true>), dim3((a.n_multi + n_pairs) * a.n_heads), block, 0, s, a);
   } else {
     hipLaunchKernelGGL((attention_kernel4<T, HD>), dim3(n_tiles * a.n_heads), dim3(256), 0, s, a);
